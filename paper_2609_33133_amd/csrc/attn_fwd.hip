@@ -1,0 +1,207 @@
+// Forward attention kernel for gfx950: prompt prefill, fused response replay
+// and the split-mode partials (§3.2, Eq. 1, §3.3).
+//
+// One workgroup = 4 wavefronts = one query tile of up to 128 rows of one
+// query head; each wavefront owns 32 query rows (one per lane column of the
+// S^T accumulator). The tile sweeps 64-key blocks of segment A (the prompt
+// KV, every key visible) and then of segment B (causal). Continuing the
+// online softmax across the two segments is the log-sum-exp merge of the two
+// partial states done in registers; a tile with only one segment produces one
+// partial state (split mode).
+//
+// Per 64-key block and wavefront: 16 MFMAs for S^T = K Q^T (K from LDS, Q^T
+// held in registers), the online-softmax update in fp32 with exp2, and 16
+// MFMAs for O^T += V^T P^T (V^T from LDS, P^T straight from the S^T
+// accumulators rounded to bf16). K and V^T are double-buffered in LDS and
+// prefetched through registers one block ahead.
+#include "common.h"
+#include "kernels.h"
+
+namespace augtree {
+
+namespace {
+
+constexpr int BM = 128;  // query rows per workgroup
+constexpr int BN = 64;   // keys per block
+
+template <int D>
+struct FwdLds {
+  static constexpr int KSTR = D + 8;   // K row stride (elements): 16-byte pad
+  static constexpr int VSTR = BN + 8;  // V^T row stride (elements)
+  __bf16 k[2][BN * KSTR];
+  __bf16 vt[2][D * VSTR];
+};
+
+template <int D, bool OUT32>
+__global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
+  using L = FwdLds<D>;
+  __shared__ L sm;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
+  const int tile_id = blockIdx.x / p.hq;
+  const int head = blockIdx.x - tile_id * p.hq;
+  const QTile t = p.tiles[tile_id];
+  const int kvh = head / p.group;
+  const int qi = wave * 32 + l32;
+  const bool qvalid = qi < t.q_len;
+  const int64_t qrow = (int64_t)t.q_row0 + qi;
+  const int64_t qstride = (int64_t)p.hq * D;
+  const int64_t kvstride = (int64_t)p.hkv * D;
+
+  // Q^T operand (B of S^T = K Q^T): lane holds query qi, d = 16*ks + 8*hf .. +7
+  bf16x8 qreg[D / 16];
+  {
+    const uint16_t* qp = p.q + qrow * qstride + head * D + hf * 8;
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks)
+      qreg[ks] = as_bf16x8(qvalid ? ldg16(qp + ks * 16) : make_uint4(0, 0, 0, 0));
+  }
+
+  const float c = p.scale_log2;
+  float m_run = -INFINITY;  // running max of raw q.k over this lane's query
+  float l_run = 0.f;        // this half-wave's share of the running sum
+  f32x16 oacc[D / 32];
+#pragma unroll
+  for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+    for (int i = 0; i < 16; ++i) oacc[db][i] = 0.f;
+
+  const int nA = (t.a_len + BN - 1) / BN;
+  const int nB = (t.b_len + BN - 1) / BN;
+  const int nblk = nA + nB;
+
+  TileStage<BN, D> kst, vst;
+  auto load_block = [&](int b) {
+    const bool isB = b >= nA;
+    const int kb0 = (isB ? b - nA : b) * BN;
+    const int len = isB ? t.b_len : t.a_len;
+    const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
+    const int nvalid = min(BN, len - kb0);
+    kst.load(isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
+    vst.load(isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
+  };
+  auto store_block = [&](int buf) {
+    kst.template store_rows<L::KSTR>(sm.k[buf]);
+    vst.template store_transposed<L::VSTR>(sm.vt[buf]);
+  };
+
+  if (nblk > 0) {
+    load_block(0);
+    store_block(0);
+  }
+  __syncthreads();
+
+  for (int b = 0; b < nblk; ++b) {
+    const int buf = b & 1;
+    if (b + 1 < nblk) load_block(b + 1);
+
+    const bool isB = b >= nA;
+    const int kb0 = (isB ? b - nA : b) * BN;
+    const int len = isB ? t.b_len : t.a_len;
+    // causal: the wavefront's smallest / largest query position
+    const int qpos_lo = t.b_qpos + wave * 32;
+    const bool skip = isB && (kb0 > qpos_lo + 31);
+    if (!skip) {
+      const __bf16* ks_lds = sm.k[buf];
+      f32x16 s0, s1;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; }
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks) {
+        const bf16x8 a0 = lds_bf16x8(ks_lds + l32 * L::KSTR + ks * 16 + hf * 8);
+        const bf16x8 a1 = lds_bf16x8(ks_lds + (32 + l32) * L::KSTR + ks * 16 + hf * 8);
+        s0 = mfma32(a0, qreg[ks], s0);
+        s1 = mfma32(a1, qreg[ks], s1);
+      }
+      const bool need_mask = (kb0 + BN > len) || (isB && (kb0 + BN - 1 > qpos_lo));
+      if (need_mask) {
+        const int qpos = t.b_qpos + qi;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int k0 = kb0 + acc_row(i, hf);
+          const int k1 = k0 + 32;
+          const bool bad0 = (k0 >= len) || (isB && k0 > qpos);
+          const bool bad1 = (k1 >= len) || (isB && k1 > qpos);
+          s0[i] = bad0 ? -INFINITY : s0[i];
+          s1[i] = bad1 ? -INFINITY : s1[i];
+        }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m_run, mx);
+      const float ms = (mnew == -INFINITY) ? 0.f : mnew * c;
+      const float alpha = __builtin_amdgcn_exp2f(m_run * c - ms);
+      m_run = mnew;
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+      float lsum = 0.f;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        s0[i] = __builtin_amdgcn_exp2f(s0[i] * c - ms);
+        s1[i] = __builtin_amdgcn_exp2f(s1[i] * c - ms);
+        lsum += s0[i] + s1[i];
+      }
+      l_run += lsum;
+      const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
+      const bf16x8 pb2 = to_bf16x8(s1, 0), pb3 = to_bf16x8(s1, 8);
+      const __bf16* vt_lds = sm.vt[buf];
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db) {
+        const __bf16* vrow = vt_lds + (db * 32 + l32) * L::VSTR + hf * 8;
+        oacc[db] = mfma32(lds_bf16x8(vrow + 0), pb0, oacc[db]);
+        oacc[db] = mfma32(lds_bf16x8(vrow + 16), pb1, oacc[db]);
+        oacc[db] = mfma32(lds_bf16x8(vrow + 32), pb2, oacc[db]);
+        oacc[db] = mfma32(lds_bf16x8(vrow + 48), pb3, oacc[db]);
+      }
+    }
+    if (b + 1 < nblk) store_block(buf ^ 1);
+    __syncthreads();
+  }
+
+  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  if (qvalid) {
+    const float inv = 1.f / l_tot;
+    const int64_t obase = qrow * qstride + head * D;
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+#pragma unroll
+      for (int g4 = 0; g4 < 4; ++g4) {
+        const int d0 = db * 32 + g4 * 8 + hf * 4;
+        const float v0 = oacc[db][g4 * 4 + 0] * inv, v1 = oacc[db][g4 * 4 + 1] * inv;
+        const float v2 = oacc[db][g4 * 4 + 2] * inv, v3 = oacc[db][g4 * 4 + 3] * inv;
+        if constexpr (OUT32) {
+          *reinterpret_cast<float4*>(p.o32 + obase + d0) = make_float4(v0, v1, v2, v3);
+        } else {
+          typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
+          bf16x4 w;
+          w[0] = (__bf16)v0; w[1] = (__bf16)v1; w[2] = (__bf16)v2; w[3] = (__bf16)v3;
+          *reinterpret_cast<bf16x4*>(p.o + obase + d0) = w;
+        }
+      }
+    }
+    if (hf == 0) p.lse[(int64_t)head * p.lse_rows + qrow] = (m_run * c + __log2f(l_tot)) * kLn2;
+  }
+}
+
+}  // namespace
+
+hipError_t launch_attn_fwd(const FwdParams& p, int n_tiles, bool out_f32, hipStream_t stream) {
+  if (n_tiles == 0) return hipSuccess;
+  const dim3 grid((unsigned)n_tiles * (unsigned)p.hq), block(256);
+  if (p.head_dim == 128) {
+    if (out_f32) hipLaunchKernelGGL((attn_fwd_kernel<128, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((attn_fwd_kernel<128, false>), grid, block, 0, stream, p);
+  } else {
+    if (out_f32) hipLaunchKernelGGL((attn_fwd_kernel<64, true>), grid, block, 0, stream, p);
+    else hipLaunchKernelGGL((attn_fwd_kernel<64, false>), grid, block, 0, stream, p);
+  }
+  return hipGetLastError();
+}
+
+int fwd_block_m() { return BM; }
+
+}  // namespace augtree

@@ -1,0 +1,218 @@
+"""GPU parity: every entry point of the C ABI against the fp64 oracle on the
+same seeded bf16 inputs (small shapes that span several tiles and a ragged
+tail; edge cases; closed-form mask probe; determinism; fused vs split)."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import attention as A
+from paper_2609_33133_amd import api
+from paper_2609_33133_amd import inputs as I
+from paper_2609_33133_amd.api import REPLAY_FUSED, REPLAY_SPLIT, GroupBatch
+from paper_2609_33133_amd.group_attention import SharedStep, upload
+
+from gpu_helpers import assert_close, log, oracle, rel, run_flattened, run_shared, to_np
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _device():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2609_33133_amd import _lib
+    lib = _lib.load()
+    assert lib.augtree_check_device() == 0, lib.augtree_last_error()
+
+
+@pytest.mark.parametrize("mode", [REPLAY_FUSED, REPLAY_SPLIT])
+def test_tiny_workload_full_parity(mode):
+    gi = I.make_config("tiny")
+    ref = oracle(gi)
+    got, _ = run_shared(gi, mode=mode)
+    assert_close(got, ref, f"tiny mode={mode}")
+
+
+SHAPES = [
+    # (prompt lens, branch lens, hq, hkv, d, qk_mult)
+    ([300], [[200, 77, 129]], 8, 2, 128, None),
+    ([130, 64], [[1, 65], [128, 3, 200]], 4, 4, 64, None),
+    ([257], [[31, 256]], 8, 2, 128, 1.0),            # sharp logits
+    ([1, 2], [[1, 300], [5]], 4, 1, 128, 1.0),        # P = 1, R = 1, MQA
+    ([64, 128, 192], [[64], [128], [192, 1]], 8, 2, 64, 1.0),
+    ([500], [[40, 41, 42, 43]], 4, 2, 128, 4.0),      # very sharp
+]
+
+
+@pytest.mark.parametrize("case", range(len(SHAPES)))
+def test_small_shapes(case):
+    ps, rs, hq, hkv, d, mult = SHAPES[case]
+    shape = I.custom_shape(ps, rs, hq, hkv, d)
+    gi = I.make_inputs(shape, seed=100 + case, qk_mult=mult)
+    log(f"case {case}: P={ps} R={rs} hq={hq} hkv={hkv} d={d} mult={mult}")
+    ref = oracle(gi)
+    for mode in (REPLAY_FUSED, REPLAY_SPLIT):
+        got, _ = run_shared(gi, mode=mode)
+        assert_close(got, ref, f"case {case} mode {mode}")
+
+
+@pytest.mark.parametrize("seed", [0, 1, 2, 3])
+def test_random_ragged_shapes(seed):
+    rng = np.random.default_rng(1000 + seed)
+    shape = I.random_shape(rng, max_groups=3, max_p=400, max_g=4, max_r=300,
+                           heads=((4, 4, 64), (8, 2, 128), (4, 1, 128)))
+    gi = I.make_inputs(shape, seed=2000 + seed, qk_mult=1.0 if seed % 2 else None)
+    log(f"seed {seed}: P={shape.prompt_lens} R={shape.branch_lens} h={shape.num_q_heads}/{shape.num_kv_heads} "
+        f"d={shape.head_dim}")
+    ref = oracle(gi)
+    got, _ = run_shared(gi, n_seed=1 + seed)
+    assert_close(got, ref, f"random {seed}")
+
+
+def test_q_zero_probe_closed_form():
+    """Q = 0: LSE = ln(#visible keys), O[..., 0] = mean of visible position labels."""
+    shape = I.custom_shape([100, 37], [[64, 1, 100], [20, 90]], 8, 2, 128)
+    gi = I.make_inputs(shape, seed=7)
+    gi.q_p[:] = 0
+    gi.q_r[:] = 0
+    for g in range(shape.num_groups):
+        p0, p1 = shape.cu_prompt[g], shape.cu_prompt[g + 1]
+        gi.v_p[p0:p1, :, 0] = I.f32_to_bf16_bits(np.arange(p1 - p0, dtype=np.float32))[:, None]
+        for b in range(shape.cu_branch[g], shape.cu_branch[g + 1]):
+            r0, r1 = shape.cu_resp[b], shape.cu_resp[b + 1]
+            gi.v_r[r0:r1, :, 0] = I.f32_to_bf16_bits((p1 - p0 + np.arange(r1 - r0)).astype(np.float32))[:, None]
+    for mode in (REPLAY_FUSED, REPLAY_SPLIT):
+        got, _ = run_shared(gi, mode=mode)
+        for g in range(shape.num_groups):
+            p0, p1 = shape.cu_prompt[g], shape.cu_prompt[g + 1]
+            P = p1 - p0
+            pos = np.arange(P)
+            assert np.max(np.abs(got["lse_p"][:, p0:p1] - np.log(pos + 1))) < 1e-5
+            assert rel(got["o_p"][p0:p1, :, 0], np.broadcast_to((pos / 2)[:, None], (P, 8))) < 1e-2
+            for b in range(shape.cu_branch[g], shape.cu_branch[g + 1]):
+                r0, r1 = shape.cu_resp[b], shape.cu_resp[b + 1]
+                t = np.arange(r1 - r0)
+                assert np.max(np.abs(got["lse_r"][:, r0:r1] - np.log(P + t + 1))) < 1e-5
+                want = np.broadcast_to(((P + t) / 2)[:, None], (r1 - r0, 8))
+                assert rel(got["o_r"][r0:r1, :, 0], want) < 1e-2
+
+
+def test_fused_equals_split():
+    shape = I.custom_shape([333, 70], [[100, 200], [65, 1, 129]], 8, 2, 128)
+    gi = I.make_inputs(shape, seed=8, qk_mult=1.0)
+    a, _ = run_shared(gi, mode=REPLAY_FUSED)
+    b, _ = run_shared(gi, mode=REPLAY_SPLIT)
+    assert rel(a["o_r"], b["o_r"]) < 2e-3
+    assert np.max(np.abs(a["lse_r"] - b["lse_r"])) < 1e-4
+    for k in ("dq_r", "dk_r", "dv_r", "dk_p", "dv_p"):
+        assert rel(a[k], b[k]) < 5e-3, k
+
+
+def test_determinism_bitwise():
+    shape = I.custom_shape([300, 90], [[100, 200, 5], [65, 129]], 8, 2, 128)
+    gi = I.make_inputs(shape, seed=9)
+    b = GroupBatch.from_shape(shape)
+    x = upload(gi)
+    outs = []
+    for _ in range(3):
+        step = SharedStep(b, "cuda", n_seed=3)
+        step.run(x)
+        torch.cuda.synchronize()
+        outs.append({k: v.clone() for k, v in step.outputs().items()})
+    for o in outs[1:]:
+        for k in o:
+            assert torch.equal(o[k].view(torch.uint8) if o[k].dtype != torch.float32 else o[k],
+                               outs[0][k].view(torch.uint8) if o[k].dtype != torch.float32 else outs[0][k]), k
+
+
+@pytest.mark.parametrize("n_seed", [1, 2, 5])
+def test_seed_chunks_give_same_prompt_gradient(n_seed):
+    shape = I.custom_shape([200], [[150, 150, 40, 300]], 8, 2, 128)
+    gi = I.make_inputs(shape, seed=10)
+    ref = oracle(gi)
+    got, step = run_shared(gi, n_seed=n_seed)
+    assert_close(got, ref, f"n_seed={n_seed}")
+    # every slab holds its chunk's contribution; their sum is the branch total
+    sh = A.shared_fwd_bwd(shape.cu_prompt, shape.cu_branch, shape.cu_resp, 8, 2, shape.scale,
+                          *(I.bf16_bits_to_f64(getattr(gi, n)) for n in ("q_p", "k_p", "v_p", "q_r", "k_r", "v_r",
+                                                                          "do_p", "do_r")))
+    seeds = to_np(step.seed).sum(0)
+    assert rel(seeds[0], sh["seed_k"].sum(0)) < 2e-2
+    assert rel(seeds[1], sh["seed_v"].sum(0)) < 2e-2
+    assert rel(to_np(step.dkv_self[0]), sh["dk_p_self"]) < 2e-2
+
+
+def test_lse_merge_entry_point():
+    rng = np.random.default_rng(11)
+    n, rows, heads, d = 3, 257, 4, 64
+    o = rng.standard_normal((n, rows, heads, d)).astype(np.float32)
+    l = (rng.standard_normal((n, heads, rows)) * 3).astype(np.float32)
+    l[1, 0, :50] = -np.inf                  # an empty part
+    l[:, 1, 7] = -np.inf                    # a row with every part empty
+    to = torch.from_numpy(o).cuda()
+    tl = torch.from_numpy(l).cuda()
+    ob, of, lse = api.lse_merge(to, tl)
+    ob2, of2, lse2 = api.lse_merge(to, tl, want_bf16=False)
+    torch.cuda.synchronize()
+    ro, rl = A.lse_merge(o.astype(np.float64).transpose(0, 2, 1, 3), l.astype(np.float64))
+    ro = ro.transpose(1, 0, 2)
+    got_f = to_np(of2)
+    got_l = to_np(lse2)
+    fin = np.isfinite(rl)
+    assert np.array_equal(np.isfinite(got_l), fin)
+    assert np.max(np.abs(got_l[fin] - rl[fin])) < 1e-5
+    assert np.all(got_f[7, 1] == 0)
+    assert rel(got_f, ro) < 1e-5
+    assert rel(to_np(ob), ro) < 1e-2
+
+
+def test_prompt_grad_reduce_bitexact_fp32():
+    """fp32 sum in index order (self first): equal bit for bit to the same
+    sequence of float32 additions on the host."""
+    rng = np.random.default_rng(12)
+    n, rows, heads, d = 5, 300, 2, 64
+    parts = rng.standard_normal((n, 2, rows, heads, d)).astype(np.float32)
+    selfp = rng.standard_normal((2, rows, heads, d)).astype(np.float32)
+    out_b, out_f = api.prompt_grad_reduce(torch.from_numpy(parts).cuda(), self_part=torch.from_numpy(selfp).cuda(),
+                                          want_bf16=False)
+    torch.cuda.synchronize()
+    exp = selfp.copy()
+    for k in range(n):
+        exp = (exp + parts[k]).astype(np.float32)
+    assert np.array_equal(out_f.cpu().numpy(), exp)
+    # row map over one shared slab, with absent rows
+    slab = rng.standard_normal((2, 50, heads, d)).astype(np.float32)
+    rm = np.full((3, 20), -1, np.int32)
+    rm[0] = np.arange(20)
+    rm[1, :10] = np.arange(30, 40)
+    rm[2, 5:] = np.arange(35, 50)
+    _, got = api.prompt_grad_reduce(torch.from_numpy(slab).cuda(), row_map=torch.from_numpy(rm).cuda(), rows=20,
+                                    shared_slab=True, n_parts=3, want_bf16=False)
+    torch.cuda.synchronize()
+    exp = np.zeros((2, 20, heads, d), np.float32)
+    for k in range(3):
+        for r in range(20):
+            if rm[k, r] >= 0:
+                exp[:, r] = (exp[:, r] + slab[:, rm[k, r]]).astype(np.float32)
+    assert np.array_equal(got.cpu().numpy(), exp)
+
+
+def test_prefill_bwd_fp32_dq_matches_bf16():
+    shape = I.custom_shape([190, 64], [[1], [1]], 8, 2, 128)
+    gi = I.make_inputs(shape, seed=13)
+    b = GroupBatch.from_shape(shape)
+    x = upload(gi)
+    o, lse = api.prefill_fwd(b, x["q_p"], x["k_p"], x["v_p"])
+    dqb, _, s1 = api.prefill_bwd(b, x["q_p"], x["k_p"], x["v_p"], o, lse, x["do_p"])
+    _, dqf, s2 = api.prefill_bwd(b, x["q_p"], x["k_p"], x["v_p"], o, lse, x["do_p"], want_bf16=False)
+    torch.cuda.synchronize()
+    assert torch.equal(dqf.to(torch.bfloat16), dqb)
+    assert torch.equal(s1, s2)
+
+
+def test_flattened_baseline_matches_oracle():
+    shape = I.custom_shape([150, 60], [[100, 33], [20, 64, 7, 129]], 8, 2, 128)
+    gi = I.make_inputs(shape, seed=14, qk_mult=1.0)
+    ref = oracle(gi)
+    got = run_flattened(gi)
+    assert_close(got, ref, "flattened")
