@@ -1,0 +1,288 @@
+"""Throughput of shared-prompt group attention (forward + backward) on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload prompt]
+
+One step = one pass of the whole hot path over one batch of synthetic input
+already resident in HBM: prefill_fwd, replay_fwd, replay_bwd, prefill_bwd and
+the Eq. 2 prompt_grad_reduce. The value is counted fwd+bwd TFLOP/s with the
+FlashAttention-2 convention 14 * d * Hq * (valid query-key pairs of the shared
+form: prefill + replay prompt column + replay own-branch blocks); the
+flattened baseline's recomputed prompt and masked-out pairs are never counted.
+
+Also reported on the same JSON line: % of the bf16 dense MFMA peak, the
+wall-time speedup over the flattened per-branch baseline built from the same
+kernels, a roofline entry for the dominant kernel (per-launch HIP-event
+durations taken around each launch by the library's launch hook, on the
+stream the kernel runs on), and the fp64 CPU oracle timed on a bounded sample
+of the same workload (cpu_baseline).
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0       # MI355X HBM3E
+METRIC = "shared-prompt attn fwd+bwd TFLOP/s, % bf16 MFMA peak, speedup vs flattened"
+
+WORKLOAD_TEXT = {
+    "tiny": "tiny group: 1 prompt, P=256, G=2, R=128, Hq=Hkv=4, d=64, seed 0",
+    "balanced": "balanced: 4 groups x (P=4096, G=8, R=4096), Hq=32, Hkv=8, d=128, seed 0",
+    "prompt": "prompt-dominant: 1 group, P=32768, G=8, R=2048, Hq=32, Hkv=8, d=128, seed 0",
+    "response": "response-dominant: 1 group, P=2048, G=16, R=16384, Hq=32, Hkv=8, d=128, seed 0",
+    "ragged": "ragged: 16 groups, P log-uniform [512,65536], G in {4,8,16}, R log-uniform [256,32768], "
+              "<=1,048,576 tokens, Hq=32, Hkv=8, d=128, seed 7",
+}
+
+# launch role -> compiled kernel (template instantiation) it runs
+ROLE_KERNEL = {
+    "fwd_prefill": "attn_fwd_kernel<bf16 out>", "fwd_replay": "attn_fwd_kernel<bf16 out>",
+    "fwd_replay_prompt": "attn_fwd_kernel<fp32 out>", "fwd_replay_own": "attn_fwd_kernel<fp32 out>",
+    "dkv_seed": "attn_dkv_kernel<fp32 out>", "dkv_prefill": "attn_dkv_kernel<fp32 out>",
+    "dkv_resp": "attn_dkv_kernel<bf16 out>",
+    "dq_replay": "attn_dq_kernel", "dq_prefill": "attn_dq_kernel",
+    "dsum": "bwd_dsum_kernel", "lse_merge": "lse_merge_kernel", "grad_reduce": "grad_reduce_kernel",
+}
+# flops per (valid pair, query head) each attention role performs
+ROLE_FLOPS_PER_PAIR_D = {"fwd": 4, "dkv": 8, "dq": 6}
+
+
+def role_work(role: str, shape, n_seed: int):
+    """Algorithmic work of one launch: ('flop', F) for contractions, ('byte', B)
+    for the HBM-bound kernels."""
+    vp = shape.valid_pairs()
+    hq, d = shape.num_q_heads, shape.head_dim
+    pairs = {
+        "fwd_prefill": vp["prefill"], "fwd_replay": vp["replay_prompt"] + vp["replay_resp"],
+        "fwd_replay_prompt": vp["replay_prompt"], "fwd_replay_own": vp["replay_resp"],
+        "dkv_seed": vp["replay_prompt"], "dkv_resp": vp["replay_resp"], "dkv_prefill": vp["prefill"],
+        "dq_replay": vp["replay_prompt"] + vp["replay_resp"], "dq_prefill": vp["prefill"],
+    }
+    if role in pairs:
+        per = ROLE_FLOPS_PER_PAIR_D[role.split("_")[0]]
+        return "flop", float(per * d * hq * pairs[role])
+    tp, tr, hkv = shape.total_prompt, shape.total_resp, shape.num_kv_heads
+    if role == "dsum":      # per launch (prompt and response launches averaged)
+        rows = (tp + tr) / 2.0
+        return "byte", float(rows * hq * (2 * d * 2 + 4))
+    if role == "grad_reduce":
+        e = 2 * tp * hkv * d
+        return "byte", float(e * 4 * (1 + n_seed) + e * 2)
+    if role == "lse_merge":
+        return "byte", float(tr * hq * (2 * d * 4 + 2 * 4 + d * 2 + 4))
+    raise KeyError(role)
+
+
+class KernelTimer:
+    """Records a HIP event pair around every library kernel launch (through
+    augtree_set_launch_hook) on the stream the kernel goes to."""
+
+    def __init__(self, lib):
+        import torch
+        self.torch = torch
+        self.lib = lib
+        self.events = []        # (role, start, end)
+        self._open = {}
+        from paper_2609_33133_amd._lib import LAUNCH_HOOK
+        self._cb = LAUNCH_HOOK(self._hook)
+
+    def _hook(self, role, phase, stream, user):
+        torch = self.torch
+        ext = torch.cuda.ExternalStream(stream) if stream else torch.cuda.default_stream()
+        ev = torch.cuda.Event(enable_timing=True)
+        ev.record(ext)
+        r = role.decode()
+        if phase == 0:
+            self._open[r] = ev
+        else:
+            self.events.append((r, self._open.pop(r), ev))
+
+    def __enter__(self):
+        self.lib.augtree_set_launch_hook(self._cb, None)
+        return self
+
+    def __exit__(self, *a):
+        self.lib.augtree_set_launch_hook(ctypes.cast(None, type(self._cb)), None)
+
+    def summary(self):
+        out = {}
+        for role, a, b in self.events:
+            out.setdefault(role, []).append(a.elapsed_time(b))
+        return out
+
+
+def time_steps(fn, steps: int, warmup: int):
+    import torch
+    for _ in range(warmup):
+        fn()
+    torch.cuda.synchronize()
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    t0 = time.perf_counter()
+    start.record()
+    for _ in range(steps):
+        fn()
+    end.record()
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    return start.elapsed_time(end) / steps, wall / steps * 1e3
+
+
+def cpu_baseline(gi, shared_flops: float):
+    """The fp64 oracle on one (group 0, query head 0, branch 0) flattened unit
+    of the workload, scaled to the whole job by flattened pair count."""
+    from threadpoolctl import threadpool_info
+
+    from oracle import attention as A
+    from paper_2609_33133_amd import inputs as I
+    s = gi.shape
+    c = I.bf16_bits_to_f64
+    p0, p1 = int(s.cu_prompt[0]), int(s.cu_prompt[1])
+    r0, r1 = int(s.cu_resp[0]), int(s.cu_resp[1])
+    kh = 0
+    args = [c(gi.q_p[p0:p1, :1]), c(gi.k_p[p0:p1, kh:kh + 1]), c(gi.v_p[p0:p1, kh:kh + 1]),
+            c(gi.q_r[r0:r1, :1]), c(gi.k_r[r0:r1, kh:kh + 1]), c(gi.v_r[r0:r1, kh:kh + 1]),
+            c(gi.do_p[p0:p1, :1]), c(gi.do_r[r0:r1, :1])]
+    P, R = p1 - p0, r1 - r0
+    t0 = time.perf_counter()
+    A.flattened_fwd_bwd([0, P], [0, 1], [0, R], 1, 1, s.scale, *args)
+    dt = time.perf_counter() - t0
+    unit_pairs = (P + R) * (P + R + 1) / 2
+    job_pairs = s.valid_pairs()["flattened"] * s.num_q_heads
+    est_job_s = dt * job_pairs / unit_pairs
+    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
+    return {"value": round(shared_flops / est_job_s / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+            "kind": "oracle",
+            "sample": f"flattened fp64 oracle on group 0, query head 0, branch 0 ([P={P}; R={R}], "
+                      f"{unit_pairs:.0f} pairs) in {dt:.1f} s; job time extrapolated by flattened pairs x heads "
+                      f"({job_pairs / unit_pairs:.0f} units): {est_job_s:.0f} s"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=3)
+    ap.add_argument("--workload", default="prompt", choices=sorted(WORKLOAD_TEXT))
+    ap.add_argument("--mode", default="fused", choices=("fused", "split"))
+    ap.add_argument("--n-seed", type=int, default=None)
+    ap.add_argument("--no-flattened", action="store_true")
+    ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--traffic", default=None, help="JSON file with measured HBM bytes per launch")
+    args = ap.parse_args()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path (the hot path shards by whole "
+              "groups or KV heads with no exchange inside the op); run with --gpus 1", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+
+    from paper_2609_33133_amd import _lib
+    from paper_2609_33133_amd import inputs as I
+    from paper_2609_33133_amd.api import REPLAY_FUSED, REPLAY_SPLIT, GroupBatch
+    from paper_2609_33133_amd.group_attention import FlattenedStep, SharedStep, upload
+
+    lib = _lib.load()
+    if not torch.cuda.is_available() or lib.augtree_check_device() != 0:
+        print("bench.py needs an MI355X (gfx950): " + lib.augtree_last_error().decode(), file=sys.stderr)
+        sys.exit(3)
+    torch.cuda.set_device(0)
+    print(f"[bench] building inputs: {args.workload}", file=sys.stderr, flush=True)
+    gi = I.make_config(args.workload)
+    s = gi.shape
+    b = GroupBatch.from_shape(s)
+    x = upload(gi, "cuda:0")
+    mode = REPLAY_FUSED if args.mode == "fused" else REPLAY_SPLIT
+    step = SharedStep(b, "cuda:0", mode=mode, n_seed=args.n_seed)
+    vp = s.valid_pairs()
+    counted = 14.0 * s.head_dim * s.num_q_heads * vp["shared"]
+
+    print("[bench] shared path", file=sys.stderr, flush=True)
+    ms, wall_ms = time_steps(lambda: step.run(x), args.steps, args.warmup)
+    tflops = counted / (ms * 1e-3) / 1e12
+
+    # per-kernel durations over the same number of steps
+    with KernelTimer(lib) as kt:
+        for _ in range(args.steps):
+            step.run(x)
+        torch.cuda.synchronize()
+    per_role = kt.summary()
+    kernels = {}
+    for role, times in per_role.items():
+        k = ROLE_KERNEL[role]
+        kind, work = role_work(role, s, step.n_seed)
+        e = kernels.setdefault(k, {"ms": 0.0, "launches": 0, "work": 0.0, "kind": kind})
+        e["ms"] += float(np.sum(times))
+        e["launches"] += len(times)
+        e["work"] += work * len(times)
+    dom_name, dom = max(kernels.items(), key=lambda kv: kv[1]["ms"])
+    avg_ms = dom["ms"] / dom["launches"]
+    per_launch = dom["work"] / dom["launches"]
+    if dom["kind"] == "flop":
+        achieved = per_launch / (avg_ms * 1e-3) / 1e12
+        roof = {"bound": "mfma", "achieved": round(achieved, 2), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(achieved / PEAK_BF16_TFLOPS, 4)}
+    else:
+        achieved = per_launch / (avg_ms * 1e-3) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS, "unit": "GB/s",
+                "frac": round(achieved / PEAK_HBM_GBS, 4)}
+    roof["kernel"] = dom_name
+    roof["avg_launch_ms"] = round(avg_ms, 4)
+    roof["launches_per_step"] = dom["launches"] // args.steps
+    roof["traffic"] = None
+    if args.traffic and os.path.exists(args.traffic):
+        with open(args.traffic) as f:
+            roof["traffic"] = json.load(f).get(dom_name)
+    kernel_table = {k: {"ms_per_step": round(v["ms"] / args.steps, 4),
+                        ("TFLOP/s" if v["kind"] == "flop" else "GB/s"):
+                            round(v["work"] / (v["ms"] * 1e-3) / (1e12 if v["kind"] == "flop" else 1e9), 2)}
+                    for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms"])}
+
+    n_seed = int(step.n_seed)
+    flat_ms = None
+    if not args.no_flattened:
+        print("[bench] flattened baseline", file=sys.stderr, flush=True)
+        del step
+        torch.cuda.empty_cache()
+        fstep = FlattenedStep(b, "cuda:0")
+        fstep.materialize(x)
+        flat_ms, _ = time_steps(fstep.run, args.steps, args.warmup)
+        del fstep
+        torch.cuda.empty_cache()
+
+    cpu = None
+    if not args.no_cpu:
+        print("[bench] cpu oracle sample", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(gi, counted)
+
+    line = {
+        "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
+        "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "replay_mode": args.mode,
+                   "n_seed": n_seed,
+                   "counted_tflop_per_step": round(counted / 1e12, 4), "flop_convention": "14*d*Hq*valid_pairs"},
+        "pct_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "speedup_vs_flattened": None if flat_ms is None else round(flat_ms / ms, 3),
+        "flattened_ms_per_step": None if flat_ms is None else round(flat_ms, 4),
+        "host_wall_ms_per_step": round(wall_ms, 4),
+        "roofline": roof,
+        "kernels": kernel_table,
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -219,6 +219,20 @@ int augtree_prompt_grad_reduce(int32_t n_tensors, int64_t rows, int32_t heads, i
                                int64_t part_stride, const float* parts, const int32_t* row_map,
                                uint16_t* out, float* out_f32, void* stream);
 
+/*
+ * Launch hook (instrumentation; not part of the method). When set, `hook` is
+ * called on the calling thread immediately before (phase 0) and after
+ * (phase 1) every kernel launch the library enqueues from that thread, with a
+ * static role name ("fwd_prefill", "fwd_replay", "fwd_replay_prompt",
+ * "fwd_replay_own", "lse_merge", "dsum", "dkv_seed", "dkv_resp",
+ * "dkv_prefill", "dq_replay", "dq_prefill", "grad_reduce") and the stream the
+ * kernel is enqueued on, so that a caller can record HIP events around single
+ * kernels. The hook must not call back into the library. NULL removes it.
+ * Per thread; the library keeps no other state.
+ */
+typedef void (*augtree_launch_hook)(const char* role, int phase, void* stream, void* user);
+void augtree_set_launch_hook(augtree_launch_hook hook, void* user);
+
 /* Static text of a status code. */
 const char* augtree_status_string(int status);
 

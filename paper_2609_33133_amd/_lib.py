@@ -32,8 +32,10 @@ OP_REPLAY_BWD = 3
 EXPORTS = (
     "augtree_workspace_size", "augtree_prefill_fwd", "augtree_replay_fwd", "augtree_lse_merge",
     "augtree_replay_bwd", "augtree_prefill_bwd", "augtree_prompt_grad_reduce", "augtree_status_string",
-    "augtree_last_error", "augtree_check_device", "augtree_version",
+    "augtree_last_error", "augtree_check_device", "augtree_version", "augtree_set_launch_hook",
 )
+
+LAUNCH_HOOK = ctypes.CFUNCTYPE(None, ctypes.c_char_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p)
 
 
 class Groups(ctypes.Structure):
@@ -79,6 +81,7 @@ def _sig(lib):
         "augtree_last_error": (ctypes.c_char_p, []),
         "augtree_check_device": (ctypes.c_int, []),
         "augtree_version": (ctypes.c_char_p, []),
+        "augtree_set_launch_hook": (None, [LAUNCH_HOOK, ctypes.c_void_p]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)

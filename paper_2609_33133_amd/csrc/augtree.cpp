@@ -26,6 +26,20 @@ using namespace augtree;
 namespace {
 
 thread_local std::string g_last_error;
+thread_local augtree_launch_hook g_hook = nullptr;
+thread_local void* g_hook_user = nullptr;
+
+// Calls the launch hook around one kernel launch.
+struct HookScope {
+  const char* role;
+  hipStream_t stream;
+  HookScope(const char* r, hipStream_t s) : role(r), stream(s) {
+    if (g_hook) g_hook(role, 0, stream, g_hook_user);
+  }
+  ~HookScope() {
+    if (g_hook) g_hook(role, 1, stream, g_hook_user);
+  }
+};
 
 int fail(int status, const char* fmt, ...) {
   char buf[512];
@@ -385,6 +399,11 @@ const char* augtree_status_string(int status) {
 
 const char* augtree_last_error(void) { return g_last_error.c_str(); }
 
+void augtree_set_launch_hook(augtree_launch_hook hook, void* user) {
+  g_hook = hook;
+  g_hook_user = user;
+}
+
 int augtree_check_device(void) {
   const int st = check_device_impl();
   return st == AUGTREE_OK ? ok() : st;
@@ -427,7 +446,10 @@ int augtree_prefill_fwd(const augtree_groups* grp, const uint16_t* q_p, const ui
   p.o = o_p; p.lse = lse_p; p.lse_rows = s.tp;
   p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d;
   p.scale_log2 = log2e_scale(s.scale);
-  if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), false, str), "prefill fwd launch"))) return st;
+  {
+    HookScope h("fwd_prefill", str);
+    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), false, str), "prefill fwd launch"))) return st;
+  }
   return ok();
 }
 
@@ -455,20 +477,32 @@ int augtree_replay_fwd(const augtree_groups* grp, int mode, const uint16_t* q_r,
   if (mode == AUGTREE_REPLAY_FUSED) {
     p.tiles = at<QTile>(ws, pl.off_q1);
     p.o = o_r; p.lse = lse_r;
-    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), false, str), "replay fwd launch"))) return st;
+    {
+      HookScope h("fwd_replay", str);
+      if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), false, str), "replay fwd launch"))) return st;
+    }
     return ok();
   }
   const int64_t part_o = s.tr * s.hq * s.d;
   const int64_t part_l = s.tr * s.hq;
   p.tiles = at<QTile>(ws, pl.off_q1);
   p.o32 = o_part; p.lse = lse_part;
-  if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), true, str), "replay prompt partial launch"))) return st;
+  {
+    HookScope h("fwd_replay_prompt", str);
+    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), true, str), "replay prompt partial launch"))) return st;
+  }
   p.tiles = at<QTile>(ws, pl.off_q2);
   p.o32 = o_part + part_o; p.lse = lse_part + part_l;
-  if ((st = hip_status(launch_attn_fwd(p, (int)pl.q2.size(), true, str), "replay own partial launch"))) return st;
-  if ((st = hip_status(launch_lse_merge(s.tr, s.hq, s.d, 2, o_part, lse_part, o_r, nullptr, lse_r, str),
-                       "lse merge launch")))
-    return st;
+  {
+    HookScope h("fwd_replay_own", str);
+    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q2.size(), true, str), "replay own partial launch"))) return st;
+  }
+  {
+    HookScope h("lse_merge", str);
+    if ((st = hip_status(launch_lse_merge(s.tr, s.hq, s.d, 2, o_part, lse_part, o_r, nullptr, lse_r, str),
+                         "lse merge launch")))
+      return st;
+  }
   return ok();
 }
 
@@ -483,6 +517,7 @@ int augtree_lse_merge(int64_t rows, int32_t heads, int32_t head_dim, int32_t n_p
   if (!o && !o_f32) return fail(AUGTREE_ERR_INVALID_ARGUMENT, "no output (o and o_f32 both null)");
   int st;
   if ((st = check_device_impl())) return st;
+  HookScope h("lse_merge", static_cast<hipStream_t>(stream));
   if ((st = hip_status(launch_lse_merge(rows, heads, head_dim, n_parts, o_parts, lse_parts, o, o_f32, lse,
                                         static_cast<hipStream_t>(stream)),
                        "lse merge launch")))
@@ -507,7 +542,10 @@ int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uin
   hipStream_t str = static_cast<hipStream_t>(stream);
   if ((st = upload(pl, ws, str))) return st;
   float* dsum = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_dsum);
-  if ((st = hip_status(launch_bwd_dsum(o_r, do_r, dsum, s.tr, s.hq, s.d, str), "dsum launch"))) return st;
+  {
+    HookScope h("dsum", str);
+    if ((st = hip_status(launch_bwd_dsum(o_r, do_r, dsum, s.tr, s.hq, s.d, str), "dsum launch"))) return st;
+  }
   const float sl2 = log2e_scale(s.scale);
   {  // prompt seeds: prompt keys x all response rows of the group (Eq. 2 sum in registers)
     DkvParams p{};
@@ -515,6 +553,7 @@ int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uin
     p.k = k_p; p.v = v_p; p.q = q_r; p.dout = do_r; p.lse = lse_r; p.dsum = dsum;
     p.dkv32 = dkv_p_seed; p.out_rows = s.tp; p.lse_rows = s.tr;
     p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
+    HookScope h("dkv_seed", str);
     if ((st = hip_status(launch_attn_dkv(p, (int)pl.kv2.size(), true, str), "seed dkv launch"))) return st;
   }
   {  // own-branch keys, causal
@@ -523,6 +562,7 @@ int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uin
     p.k = k_r; p.v = v_r; p.q = q_r; p.dout = do_r; p.lse = lse_r; p.dsum = dsum;
     p.dk = dk_r; p.dv = dv_r; p.out_rows = s.tr; p.lse_rows = s.tr;
     p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
+    HookScope h("dkv_resp", str);
     if ((st = hip_status(launch_attn_dkv(p, (int)pl.kv1.size(), false, str), "response dkv launch"))) return st;
   }
   {  // dQ over prompt keys then own-branch keys
@@ -532,6 +572,7 @@ int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uin
     p.ka = k_p; p.va = v_p; p.kb = k_r; p.vb = v_r;
     p.dq = dq_r; p.lse_rows = s.tr;
     p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
+    HookScope h("dq_replay", str);
     if ((st = hip_status(launch_attn_dq(p, (int)pl.q1.size(), str), "replay dq launch"))) return st;
   }
   return ok();
@@ -553,7 +594,10 @@ int augtree_prefill_bwd(const augtree_groups* grp, const uint16_t* q_p, const ui
   hipStream_t str = static_cast<hipStream_t>(stream);
   if ((st = upload(pl, ws, str))) return st;
   float* dsum = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_dsum);
-  if ((st = hip_status(launch_bwd_dsum(o_p, do_p, dsum, s.tp, s.hq, s.d, str), "dsum launch"))) return st;
+  {
+    HookScope h("dsum", str);
+    if ((st = hip_status(launch_bwd_dsum(o_p, do_p, dsum, s.tp, s.hq, s.d, str), "dsum launch"))) return st;
+  }
   const float sl2 = log2e_scale(s.scale);
   {
     DkvParams p{};
@@ -561,6 +605,7 @@ int augtree_prefill_bwd(const augtree_groups* grp, const uint16_t* q_p, const ui
     p.k = k_p; p.v = v_p; p.q = q_p; p.dout = do_p; p.lse = lse_p; p.dsum = dsum;
     p.dkv32 = dkv_p_self; p.out_rows = s.tp; p.lse_rows = s.tp;
     p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
+    HookScope h("dkv_prefill", str);
     if ((st = hip_status(launch_attn_dkv(p, (int)pl.kv1.size(), true, str), "prefill dkv launch"))) return st;
   }
   {
@@ -570,6 +615,7 @@ int augtree_prefill_bwd(const augtree_groups* grp, const uint16_t* q_p, const ui
     p.ka = k_p; p.va = v_p; p.kb = k_p; p.vb = v_p;
     p.dq = dq_p; p.dq32 = dq_p_f32; p.lse_rows = s.tp;
     p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
+    HookScope h("dq_prefill", str);
     if ((st = hip_status(launch_attn_dq(p, (int)pl.q1.size(), str), "prefill dq launch"))) return st;
   }
   return ok();
@@ -593,6 +639,7 @@ int augtree_prompt_grad_reduce(int32_t n_tensors, int64_t rows, int32_t heads, i
   if (!out && !out_f32) return fail(AUGTREE_ERR_INVALID_ARGUMENT, "no output (out and out_f32 both null)");
   int st;
   if ((st = check_device_impl())) return st;
+  HookScope h("grad_reduce", static_cast<hipStream_t>(stream));
   if ((st = hip_status(launch_grad_reduce(n_tensors, rows, (int64_t)heads * head_dim, self, n_parts, part_rows,
                                           part_stride, parts, row_map, out, out_f32, static_cast<hipStream_t>(stream)),
                        "grad reduce launch")))
