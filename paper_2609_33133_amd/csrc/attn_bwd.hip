@@ -7,13 +7,15 @@
 // * attn_dq_kernel (query-outer): one workgroup per 128-row query tile and
 //   query head, sweeping the same key segments as the forward (prompt keys,
 //   then the branch's own causal keys). S^T, dP^T and dS^T keep one query per
-//   lane; dQ^T += K^T dS^T takes dS^T straight from the accumulators.
+//   lane; dQ^T += K^T dS^T takes dS^T straight from the accumulators and K^T
+//   by transpose reads of the row-major K tile.
 // * attn_dkv_kernel (key-outer): one workgroup per 128-key tile and KV head;
 //   each wavefront holds 32 keys (K and V rows in registers) and sweeps every
 //   query that sees them: the g query heads of the KV head (GQA) and, for
 //   prompt keys in replay, the response rows of every branch of the group, so
 //   the Eq. 2 sum over branches happens in the accumulators. Query tiles of 64
-//   rows are staged in LDS both row-major and transposed.
+//   rows are staged in LDS row-major; Q^T and dO^T operands come from
+//   transpose reads of the same tiles.
 #include "common.h"
 #include "kernels.h"
 
@@ -28,22 +30,21 @@ constexpr int DQ_BN = 64;
 
 template <int D>
 struct DqLds {
-  static constexpr int RSTR = D + 8;
-  static constexpr int TSTR = DQ_BN + 8;
-  __bf16 k[2][DQ_BN * RSTR];
-  __bf16 v[2][DQ_BN * RSTR];
-  __bf16 kt[2][D * TSTR];
+  __bf16 k[2][DQ_BN * D];
+  __bf16 v[2][DQ_BN * D];
 };
 
 template <int D>
 __global__ __launch_bounds__(256, 1) void attn_dq_kernel(DqParams p) {
   using L = DqLds<D>;
   __shared__ L sm;
+  int unit, hh;
+  if (!xcd_unit(p.n_units, p.group, unit, hh)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
-  const int tile_id = blockIdx.x / p.hq;
-  const int head = blockIdx.x - tile_id * p.hq;
+  const int tile_id = unit / p.hkv;
+  const int kvh = unit - tile_id * p.hkv;
+  const int head = kvh * p.group + hh;
   const QTile t = p.tiles[tile_id];
-  const int kvh = head / p.group;
   const int qi = wave * 32 + l32;
   const bool qvalid = qi < t.q_len;
   const int64_t qrow = (int64_t)t.q_row0 + qi;
@@ -84,9 +85,8 @@ __global__ __launch_bounds__(256, 1) void attn_dq_kernel(DqParams p) {
     vst.load(isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
   auto store_block = [&](int buf) {
-    kst.template store_rows<L::RSTR>(sm.k[buf]);
-    kst.template store_transposed<L::TSTR>(sm.kt[buf]);
-    vst.template store_rows<L::RSTR>(sm.v[buf]);
+    kst.store(sm.k[buf]);
+    vst.store(sm.v[buf]);
   };
 
   if (nblk > 0) {
@@ -112,10 +112,10 @@ __global__ __launch_bounds__(256, 1) void attn_dq_kernel(DqParams p) {
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
         const int col = ks * 16 + hf * 8;
-        s0 = mfma32(lds_bf16x8(kl + l32 * L::RSTR + col), qreg[ks], s0);
-        s1 = mfma32(lds_bf16x8(kl + (32 + l32) * L::RSTR + col), qreg[ks], s1);
-        d0 = mfma32(lds_bf16x8(vl + l32 * L::RSTR + col), doreg[ks], d0);
-        d1 = mfma32(lds_bf16x8(vl + (32 + l32) * L::RSTR + col), doreg[ks], d1);
+        s0 = mfma32(lds_row8<D>(kl, l32, col), qreg[ks], s0);
+        s1 = mfma32(lds_row8<D>(kl, 32 + l32, col), qreg[ks], s1);
+        d0 = mfma32(lds_row8<D>(vl, l32, col), doreg[ks], d0);
+        d1 = mfma32(lds_row8<D>(vl, 32 + l32, col), doreg[ks], d1);
       }
       const bool need_mask = (kb0 + DQ_BN > len) || (isB && (kb0 + DQ_BN - 1 > qpos_lo));
       const int qpos = t.b_qpos + qi;
@@ -133,14 +133,12 @@ __global__ __launch_bounds__(256, 1) void attn_dq_kernel(DqParams p) {
       }
       const bf16x8 g0 = to_bf16x8(s0, 0), g1 = to_bf16x8(s0, 8);
       const bf16x8 g2 = to_bf16x8(s1, 0), g3 = to_bf16x8(s1, 8);
-      const __bf16* ktl = sm.kt[buf];
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        const __bf16* row = ktl + (db * 32 + l32) * L::TSTR + hf * 8;
-        acc[db] = mfma32(lds_bf16x8(row + 0), g0, acc[db]);
-        acc[db] = mfma32(lds_bf16x8(row + 16), g1, acc[db]);
-        acc[db] = mfma32(lds_bf16x8(row + 32), g2, acc[db]);
-        acc[db] = mfma32(lds_bf16x8(row + 48), g3, acc[db]);
+        acc[db] = mfma32(lds_tr_operand<D>(kl, 0, db * 32), g0, acc[db]);
+        acc[db] = mfma32(lds_tr_operand<D>(kl, 16, db * 32), g1, acc[db]);
+        acc[db] = mfma32(lds_tr_operand<D>(kl, 32, db * 32), g2, acc[db]);
+        acc[db] = mfma32(lds_tr_operand<D>(kl, 48, db * 32), g3, acc[db]);
       }
     }
     if (b + 1 < nblk) store_block(buf ^ 1);
@@ -175,12 +173,8 @@ constexpr int KV_BQ = 64;   // query rows per block
 
 template <int D>
 struct DkvLds {
-  static constexpr int RSTR = D + 8;
-  static constexpr int TSTR = KV_BQ + 8;
-  __bf16 q[2][KV_BQ * RSTR];
-  __bf16 qt[2][D * TSTR];
-  __bf16 dout[2][KV_BQ * RSTR];
-  __bf16 doutt[2][D * TSTR];
+  __bf16 q[2][KV_BQ * D];
+  __bf16 dout[2][KV_BQ * D];
   float lse2[2][KV_BQ];
   float dsum[2][KV_BQ];
 };
@@ -233,10 +227,8 @@ __global__ __launch_bounds__(256, 1) void attn_dkv_kernel(DkvParams p) {
       stat = (tid - KV_BQ) < nvalid ? p.dsum[(int64_t)hh * p.lse_rows + row0 + tid - KV_BQ] : 0.f;
   };
   auto store_block = [&](int buf) {
-    qst.template store_rows<L::RSTR>(sm.q[buf]);
-    qst.template store_transposed<L::TSTR>(sm.qt[buf]);
-    dost.template store_rows<L::RSTR>(sm.dout[buf]);
-    dost.template store_transposed<L::TSTR>(sm.doutt[buf]);
+    qst.store(sm.q[buf]);
+    dost.store(sm.dout[buf]);
     if (tid < KV_BQ) sm.lse2[buf][tid] = stat;
     else if (tid < 2 * KV_BQ) sm.dsum[buf][tid - KV_BQ] = stat;
   };
@@ -261,12 +253,12 @@ __global__ __launch_bounds__(256, 1) void attn_dkv_kernel(DkvParams p) {
         f32x16 s, dp;
 #pragma unroll
         for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
-        const __bf16* ql = sm.q[buf] + (qs * 32 + l32) * L::RSTR + hf * 8;
-        const __bf16* dl = sm.dout[buf] + (qs * 32 + l32) * L::RSTR + hf * 8;
+        const __bf16* ql = sm.q[buf];
+        const __bf16* dl = sm.dout[buf];
 #pragma unroll
         for (int ks = 0; ks < D / 16; ++ks) {
-          s = mfma32(lds_bf16x8(ql + ks * 16), kreg[ks], s);
-          dp = mfma32(lds_bf16x8(dl + ks * 16), vreg[ks], dp);
+          s = mfma32(lds_row8<D>(ql, qs * 32 + l32, ks * 16 + hf * 8), kreg[ks], s);
+          dp = mfma32(lds_row8<D>(dl, qs * 32 + l32, ks * 16 + hf * 8), vreg[ks], dp);
         }
 #pragma unroll
         for (int g4 = 0; g4 < 4; ++g4) {
@@ -287,13 +279,10 @@ __global__ __launch_bounds__(256, 1) void attn_dkv_kernel(DkvParams p) {
         const bf16x8 gb0 = to_bf16x8(dp, 0), gb1 = to_bf16x8(dp, 8);
 #pragma unroll
         for (int db = 0; db < D / 32; ++db) {
-          const int col = qs * 32 + hf * 8;
-          const __bf16* dor = sm.doutt[buf] + (db * 32 + l32) * L::TSTR + col;
-          const __bf16* qr = sm.qt[buf] + (db * 32 + l32) * L::TSTR + col;
-          dv[db] = mfma32(pb0, lds_bf16x8(dor + 0), dv[db]);
-          dv[db] = mfma32(pb1, lds_bf16x8(dor + 16), dv[db]);
-          dk[db] = mfma32(gb0, lds_bf16x8(qr + 0), dk[db]);
-          dk[db] = mfma32(gb1, lds_bf16x8(qr + 16), dk[db]);
+          dv[db] = mfma32(pb0, lds_tr_operand<D>(sm.dout[buf], qs * 32, db * 32), dv[db]);
+          dv[db] = mfma32(pb1, lds_tr_operand<D>(sm.dout[buf], qs * 32 + 16, db * 32), dv[db]);
+          dk[db] = mfma32(gb0, lds_tr_operand<D>(sm.q[buf], qs * 32, db * 32), dk[db]);
+          dk[db] = mfma32(gb1, lds_tr_operand<D>(sm.q[buf], qs * 32 + 16, db * 32), dk[db]);
         }
       }
     }
@@ -355,9 +344,11 @@ __global__ __launch_bounds__(256) void bwd_dsum_kernel(const uint16_t* o, const 
 
 }  // namespace
 
-hipError_t launch_attn_dq(const DqParams& p, int n_tiles, hipStream_t stream) {
+hipError_t launch_attn_dq(const DqParams& p0, int n_tiles, hipStream_t stream) {
   if (n_tiles == 0) return hipSuccess;
-  const dim3 grid((unsigned)n_tiles * (unsigned)p.hq), block(256);
+  DqParams p = p0;
+  p.n_units = n_tiles * p.hkv;
+  const dim3 grid((unsigned)xcd_grid(p.n_units, p.group)), block(256);
   if (p.head_dim == 128) hipLaunchKernelGGL((attn_dq_kernel<128>), grid, block, 0, stream, p);
   else hipLaunchKernelGGL((attn_dq_kernel<64>), grid, block, 0, stream, p);
   return hipGetLastError();

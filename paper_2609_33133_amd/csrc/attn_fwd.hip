@@ -9,11 +9,13 @@
 // partial states done in registers; a tile with only one segment produces one
 // partial state (split mode).
 //
-// Per 64-key block and wavefront: 16 MFMAs for S^T = K Q^T (K from LDS, Q^T
-// held in registers), the online-softmax update in fp32 with exp2, and 16
-// MFMAs for O^T += V^T P^T (V^T from LDS, P^T straight from the S^T
-// accumulators rounded to bf16). K and V^T are double-buffered in LDS and
-// prefetched through registers one block ahead.
+// Per 64-key block and wavefront: 16 MFMAs for S^T = K Q^T (K rows from LDS,
+// Q^T held in registers), the online-softmax update in fp32 with exp2 (the
+// output is rescaled only when a row maximum grows), and 16 MFMAs for
+// O^T += V^T P^T (V^T by transpose reads of the row-major V tile, P^T straight
+// from the S^T accumulators rounded to bf16). K and V tiles are
+// double-buffered in LDS and prefetched through registers one block ahead.
+// The query heads of one KV head run on one XCD (shared K/V in its L2).
 #include "common.h"
 #include "kernels.h"
 
@@ -26,21 +28,21 @@ constexpr int BN = 64;   // keys per block
 
 template <int D>
 struct FwdLds {
-  static constexpr int KSTR = D + 8;   // K row stride (elements): 16-byte pad
-  static constexpr int VSTR = BN + 8;  // V^T row stride (elements)
-  __bf16 k[2][BN * KSTR];
-  __bf16 vt[2][D * VSTR];
+  __bf16 k[2][BN * D];
+  __bf16 v[2][BN * D];
 };
 
 template <int D, bool OUT32>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   using L = FwdLds<D>;
   __shared__ L sm;
+  int unit, hh;
+  if (!xcd_unit(p.n_units, p.group, unit, hh)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
-  const int tile_id = blockIdx.x / p.hq;
-  const int head = blockIdx.x - tile_id * p.hq;
+  const int tile_id = unit / p.hkv;
+  const int kvh = unit - tile_id * p.hkv;
+  const int head = kvh * p.group + hh;
   const QTile t = p.tiles[tile_id];
-  const int kvh = head / p.group;
   const int qi = wave * 32 + l32;
   const bool qvalid = qi < t.q_len;
   const int64_t qrow = (int64_t)t.q_row0 + qi;
@@ -80,8 +82,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     vst.load(isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
   auto store_block = [&](int buf) {
-    kst.template store_rows<L::KSTR>(sm.k[buf]);
-    vst.template store_transposed<L::VSTR>(sm.vt[buf]);
+    kst.store(sm.k[buf]);
+    vst.store(sm.v[buf]);
   };
 
   if (nblk > 0) {
@@ -97,20 +99,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
-    // causal: the wavefront's smallest / largest query position
-    const int qpos_lo = t.b_qpos + wave * 32;
+    const int qpos_lo = t.b_qpos + wave * 32;  // causal: the wavefront's first query position
     const bool skip = isB && (kb0 > qpos_lo + 31);
     if (!skip) {
-      const __bf16* ks_lds = sm.k[buf];
+      const __bf16* kl = sm.k[buf];
       f32x16 s0, s1;
 #pragma unroll
       for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const bf16x8 a0 = lds_bf16x8(ks_lds + l32 * L::KSTR + ks * 16 + hf * 8);
-        const bf16x8 a1 = lds_bf16x8(ks_lds + (32 + l32) * L::KSTR + ks * 16 + hf * 8);
-        s0 = mfma32(a0, qreg[ks], s0);
-        s1 = mfma32(a1, qreg[ks], s1);
+        const int col = ks * 16 + hf * 8;
+        s0 = mfma32(lds_row8<D>(kl, l32, col), qreg[ks], s0);
+        s1 = mfma32(lds_row8<D>(kl, 32 + l32, col), qreg[ks], s1);
       }
       const bool need_mask = (kb0 + BN > len) || (isB && (kb0 + BN - 1 > qpos_lo));
       if (need_mask) {
@@ -119,10 +119,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
         for (int i = 0; i < 16; ++i) {
           const int k0 = kb0 + acc_row(i, hf);
           const int k1 = k0 + 32;
-          const bool bad0 = (k0 >= len) || (isB && k0 > qpos);
-          const bool bad1 = (k1 >= len) || (isB && k1 > qpos);
-          s0[i] = bad0 ? -INFINITY : s0[i];
-          s1[i] = bad1 ? -INFINITY : s1[i];
+          if ((k0 >= len) || (isB && k0 > qpos)) s0[i] = -INFINITY;
+          if ((k1 >= len) || (isB && k1 > qpos)) s1[i] = -INFINITY;
         }
       }
       float mx = -INFINITY;
@@ -130,14 +128,17 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
       mx = fmaxf(mx, __shfl_xor(mx, 32));
       const float mnew = fmaxf(m_run, mx);
-      const float ms = (mnew == -INFINITY) ? 0.f : mnew * c;
-      const float alpha = __builtin_amdgcn_exp2f(m_run * c - ms);
-      m_run = mnew;
-      l_run *= alpha;
+      if (__any(mnew > m_run)) {
+        // rescale only when some row maximum of this wavefront grew
+        const float alpha = (mnew == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run - mnew) * c);
+        l_run *= alpha;
 #pragma unroll
-      for (int db = 0; db < D / 32; ++db)
+        for (int db = 0; db < D / 32; ++db)
 #pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+          for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+        m_run = mnew;
+      }
+      const float ms = (m_run == -INFINITY) ? 0.f : m_run * c;
       float lsum = 0.f;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
@@ -148,14 +149,13 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       l_run += lsum;
       const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
       const bf16x8 pb2 = to_bf16x8(s1, 0), pb3 = to_bf16x8(s1, 8);
-      const __bf16* vt_lds = sm.vt[buf];
+      const __bf16* vl = sm.v[buf];
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        const __bf16* vrow = vt_lds + (db * 32 + l32) * L::VSTR + hf * 8;
-        oacc[db] = mfma32(lds_bf16x8(vrow + 0), pb0, oacc[db]);
-        oacc[db] = mfma32(lds_bf16x8(vrow + 16), pb1, oacc[db]);
-        oacc[db] = mfma32(lds_bf16x8(vrow + 32), pb2, oacc[db]);
-        oacc[db] = mfma32(lds_bf16x8(vrow + 48), pb3, oacc[db]);
+        oacc[db] = mfma32(lds_tr_operand<D>(vl, 0, db * 32), pb0, oacc[db]);
+        oacc[db] = mfma32(lds_tr_operand<D>(vl, 16, db * 32), pb1, oacc[db]);
+        oacc[db] = mfma32(lds_tr_operand<D>(vl, 32, db * 32), pb2, oacc[db]);
+        oacc[db] = mfma32(lds_tr_operand<D>(vl, 48, db * 32), pb3, oacc[db]);
       }
     }
     if (b + 1 < nblk) store_block(buf ^ 1);
@@ -189,9 +189,11 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
 }  // namespace
 
-hipError_t launch_attn_fwd(const FwdParams& p, int n_tiles, bool out_f32, hipStream_t stream) {
+hipError_t launch_attn_fwd(const FwdParams& p0, int n_tiles, bool out_f32, hipStream_t stream) {
   if (n_tiles == 0) return hipSuccess;
-  const dim3 grid((unsigned)n_tiles * (unsigned)p.hq), block(256);
+  FwdParams p = p0;
+  p.n_units = n_tiles * p.hkv;
+  const dim3 grid((unsigned)xcd_grid(p.n_units, p.group)), block(256);
   if (p.head_dim == 128) {
     if (out_f32) hipLaunchKernelGGL((attn_fwd_kernel<128, true>), grid, block, 0, stream, p);
     else hipLaunchKernelGGL((attn_fwd_kernel<128, false>), grid, block, 0, stream, p);

@@ -2,18 +2,22 @@
 //
 // MFMA tiling used throughout: v_mfma_f32_32x32x16_bf16 (CDNA4), one 64-lane
 // wavefront per 32x32 output tile. Lane l holds A row (l % 32) / B column
-// (l % 32), eight consecutive k values at k = 8*(l / 32) .. +7. The 16
-// accumulator registers of lane l hold column (l % 32) and rows
+// (l % 32), eight k values; the 16 accumulator registers of lane l hold
+// column (l % 32) and rows
 //   row(i) = 8*(i / 4) + 4*(l / 32) + (i % 4),  i = 0..15.
 //
-// Attention is computed in the "transposed" orientation wherever a row
-// statistic is needed: S^T = K Q^T puts one query per lane (column), so the
-// row max / row sum of the online softmax are in-lane reductions plus one
-// exchange between the two half-waves. The probabilities left in the
-// accumulator registers are fed directly as the B operand of the next MFMA
-// (P^T for O^T = V^T P^T); the other operand is read from LDS with its key
-// (or query) index permuted inside each group of 16 to match the accumulator
-// row order (see kperm).
+// Row statistics of the softmax are computed in the "transposed" orientation
+// (S^T = K Q^T puts one query per lane), so row max / row sum are in-lane
+// reductions plus one exchange between the two half-waves. The values left in
+// the accumulators are fed directly as the B operand of the next MFMA: the
+// eight registers 8s..8s+7 of half-wave h cover rows 16s + 4h + {0..3} and
+// 16s + 8 + 4h + {0..3}, so the k index of that MFMA runs over those rows, and
+// the other operand is fetched from LDS in the same order with the gfx950
+// transpose read (lds_tr_operand).
+//
+// LDS tiles are row-major, unpadded, with the 16-byte chunks of row r stored
+// at chunk index (chunk ^ swz(r)): 16-byte row reads of 16 consecutive rows
+// and transpose reads of 4 consecutive rows both touch distinct banks.
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -26,6 +30,7 @@ namespace augtree {
 typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
 typedef float f32x16 __attribute__((ext_vector_type(16)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef short s16x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const f32x16& c) {
   return __builtin_amdgcn_mfma_f32_32x32x16_bf16(a, b, c, 0, 0, 0);
@@ -34,14 +39,6 @@ __device__ __forceinline__ f32x16 mfma32(const bf16x8& a, const bf16x8& b, const
 // Accumulator register i of a 32x32 tile -> row inside the tile.
 __device__ __forceinline__ int acc_row(int i, int hf) { return ((i >> 2) << 3) + (hf << 2) + (i & 3); }
 
-// Position of index k inside the LDS row of a transposed operand: inside each
-// group of 16, the 8 indices that accumulator registers 0..7 (or 8..15) of a
-// half-wave hold become contiguous, so one 16-byte LDS read feeds one MFMA.
-__device__ __forceinline__ int kperm(int k) {
-  const int k16 = k & 15;
-  return (k & ~15) | (((k16 >> 2) & 1) << 3) | ((k16 >> 3) << 2) | (k16 & 3);
-}
-
 __device__ __forceinline__ uint4 ldg16(const uint16_t* p) { return *reinterpret_cast<const uint4*>(p); }
 
 __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) {
@@ -49,8 +46,6 @@ __device__ __forceinline__ bf16x8 as_bf16x8(const uint4& v) {
   __builtin_memcpy(&r, &v, 16);
   return r;
 }
-
-__device__ __forceinline__ bf16x8 lds_bf16x8(const __bf16* p) { return *reinterpret_cast<const bf16x8*>(p); }
 
 // Eight fp32 -> bf16 (round to nearest even; v_cvt_pk_bf16_f32 on gfx950).
 __device__ __forceinline__ bf16x8 to_bf16x8(const f32x16& v, int base) {
@@ -72,18 +67,62 @@ __device__ __forceinline__ uint32_t half16(const uint4& v, int e) {
   return (e & 1) ? (x >> 16) : (x & 0xffffu);
 }
 
-// Register-staged copy of a tile of ROWS rows x D bf16 columns into LDS, both
-// row-major (row stride RSTR elements) and, optionally, transposed with the
-// row index permuted by kperm (row stride TSTR elements). 256 threads; thread
-// t owns rows (t / CH) * RPT .. +RPT-1 and 16-byte column chunk t % CH.
+// ---------------------------------------------------------------------------- swizzled LDS tiles
+
+template <int D>
+__device__ __forceinline__ int swz(int row) {
+  if constexpr (D == 128) return ((row & 7) << 1) | ((row >> 3) & 1);  // 16 chunks per row
+  else return (row >> 1) & 7;                                            // 8 chunks per row
+}
+
+// element offset of (row, col) in a swizzled [*, D] tile; col % 4 == 0 keeps
+// 8-byte accesses inside one chunk
+template <int D>
+__device__ __forceinline__ int toff(int row, int col) {
+  return row * D + ((((col >> 3) ^ swz<D>(row))) << 3) + (col & 7);
+}
+
+// 16-byte read of columns c .. c+7 (c % 8 == 0) of `row`
+template <int D>
+__device__ __forceinline__ bf16x8 lds_row8(const __bf16* tile, int row, int c) {
+  return *reinterpret_cast<const bf16x8*>(tile + toff<D>(row, c));
+}
+
+__device__ __forceinline__ s16x4 lds_tr16(const __bf16* p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
+}
+
+// MFMA operand whose k index runs along the rows of a swizzled tile: lane l
+// gets column c0 + (l % 32) at rows r0 + 4*(l/32) + {0,1,2,3} (elements 0..3)
+// and r0 + 8 + 4*(l/32) + {0,1,2,3} (elements 4..7), i.e. exactly the rows
+// that accumulator registers 8s..8s+7 of the same half-wave hold when
+// r0 = 16 s. Two ds_read_b64_tr_b16: inside each 16-lane group, lane j
+// addresses 4 columns of row (j / 4) and receives one column of 4 rows.
+template <int D>
+__device__ __forceinline__ bf16x8 lds_tr_operand(const __bf16* tile, int r0, int c0) {
+  const int lane = threadIdx.x & 63;
+  const int grp = lane >> 4, j = lane & 15;
+  const int col = c0 + 16 * (grp & 1) + 4 * (j & 3);
+  const int row = r0 + 4 * (grp >> 1) + (j >> 2);
+  const s16x4 a = lds_tr16(tile + toff<D>(row, col));
+  const s16x4 b = lds_tr16(tile + toff<D>(row + 8, col));
+  bf16x8 r;
+  __builtin_memcpy(&r, &a, 8);
+  __builtin_memcpy(reinterpret_cast<char*>(&r) + 8, &b, 8);
+  return r;
+}
+
+// Register-staged copy of a ROWS x D bf16 tile into a swizzled LDS tile. 256
+// threads; thread t owns rows (t / CH) * RPT .. +RPT-1 and chunk t % CH.
 template <int ROWS, int D>
 struct TileStage {
   static constexpr int CH = D / 8;
   static constexpr int RPT = ROWS * CH / 256;
-  static_assert(RPT >= 1 && (RPT == 1 || RPT == 2 || RPT == 4), "rows per thread");
+  static_assert(RPT >= 1, "rows per thread");
   uint4 r[RPT];
 
-  // rows row0 .. row0+nvalid-1 of a [*, stride] bf16 tensor, column offset col0
+  // rows row0 .. row0+nvalid-1 of a [*, stride] bf16 tensor, column offset col0;
+  // rows past nvalid are zero
   __device__ __forceinline__ void load(const uint16_t* base, int64_t row0, int nvalid, int64_t stride,
                                        int col0) {
     const int tid = threadIdx.x;
@@ -98,35 +137,31 @@ struct TileStage {
     }
   }
 
-  template <int RSTR>
-  __device__ __forceinline__ void store_rows(__bf16* lds) const {
+  __device__ __forceinline__ void store(__bf16* lds) const {
     const int tid = threadIdx.x;
     const int rg = tid / CH, dc = tid % CH;
 #pragma unroll
-    for (int j = 0; j < RPT; ++j)
-      *reinterpret_cast<uint4*>(lds + (rg * RPT + j) * RSTR + dc * 8) = r[j];
-  }
-
-  template <int TSTR>
-  __device__ __forceinline__ void store_transposed(__bf16* lds) const {
-    const int tid = threadIdx.x;
-    const int rg = tid / CH, dc = tid % CH;
-    const int pos = kperm(rg * RPT);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      __bf16* dst = lds + (dc * 8 + e) * TSTR + pos;
-      if constexpr (RPT == 4) {
-        uint2 w;
-        w.x = half16(r[0], e) | (half16(r[1], e) << 16);
-        w.y = half16(r[2], e) | (half16(r[3], e) << 16);
-        *reinterpret_cast<uint2*>(dst) = w;
-      } else if constexpr (RPT == 2) {
-        *reinterpret_cast<uint32_t*>(dst) = half16(r[0], e) | (half16(r[1], e) << 16);
-      } else {
-        *reinterpret_cast<uint16_t*>(dst) = (uint16_t)half16(r[0], e);
-      }
+    for (int j = 0; j < RPT; ++j) {
+      const int row = rg * RPT + j;
+      *reinterpret_cast<uint4*>(lds + toff<D>(row, dc * 8)) = r[j];
     }
   }
 };
+
+// ---------------------------------------------------------------------------- workgroup order
+
+// Workgroups are dispatched round-robin over the 8 XCDs (id % 8), each with
+// its own L2. Units of `per_unit` consecutive workgroups (the query heads of
+// one KV head on one tile) are kept on one XCD, and units are dealt to XCDs
+// in schedule order (heaviest first). Returns false for padding workgroups.
+__device__ __forceinline__ bool xcd_unit(int n_units, int per_unit, int& unit, int& sub) {
+  const int i = blockIdx.x;
+  const int x = i & 7, j = i >> 3;
+  unit = (j / per_unit) * 8 + x;
+  sub = j % per_unit;
+  return unit < n_units;
+}
+
+__host__ __device__ inline int xcd_grid(int n_units, int per_unit) { return ((n_units + 7) / 8) * 8 * per_unit; }
 
 }  // namespace augtree

@@ -21,6 +21,7 @@ struct FwdParams {
   int64_t lse_rows;
   int hq, hkv, group, head_dim;
   float scale_log2;    // softmax_scale * log2(e)
+  int n_units;         // tiles x KV heads (set by the launcher)
 };
 
 struct DqParams {
@@ -38,6 +39,7 @@ struct DqParams {
   int64_t lse_rows;
   int hq, hkv, group, head_dim;
   float scale, scale_log2;
+  int n_units;         // tiles x KV heads (set by the launcher)
 };
 
 struct DkvParams {
