@@ -24,9 +24,13 @@ Offsets: cu_prompt [num_groups+1] (prompt rows of group g),
 cu_branch [num_groups+1] (group g owns branches cu_branch[g]..cu_branch[g+1]),
 cu_resp [num_branches+1] (response rows of branch b).
 
-Draw order for tensors: Q_P, K_P, V_P, Q_R, K_R, V_R, dO_P, dO_R, each from
-``standard_normal(float32)`` over the packed array; Q, K, V are multiplied by
-1/sqrt(d) in fp32 and dO is not scaled; fp32 -> bf16 by round-to-nearest-even.
+Tensors: Q_P, K_P, V_P, Q_R, K_R, V_R, dO_P, dO_R (tensor index 0..7). Each
+packed array is cut into chunks of CHUNK_ROWS rows; chunk c of tensor t is
+``standard_normal(float32)`` from its own PCG64 stream seeded with
+``SeedSequence([seed, t, c])`` (independent streams, drawn in parallel
+threads). Q, K, V are multiplied by 1/sqrt(d) in fp32, dO is not scaled;
+fp32 -> bf16 by round-to-nearest-even. The ragged lengths are drawn first from
+the main stream ``PCG64(seed)``.
 """
 from __future__ import annotations
 
@@ -162,20 +166,34 @@ def bf16_bits_to_f64(b: np.ndarray) -> np.ndarray:
     return bf16_bits_to_f32(b).astype(np.float64)
 
 
-def _draw_bf16(rng: np.random.Generator, shape, mult: Optional[float], chunk_rows: int = 8192) -> np.ndarray:
-    """standard_normal(float32) over a packed [rows, ...] array, optionally times
-    `mult` in fp32, rounded to bf16. Drawn in row chunks; the stream is the same
-    as one draw of the whole array."""
+CHUNK_ROWS = 2048
+
+
+def _round_bf16(x: np.ndarray) -> np.ndarray:
+    """fp32 -> bf16 bits, round to nearest even (torch's conversion; equal to
+    ``f32_to_bf16_bits``, which the tests pin)."""
+    import torch
+    return torch.from_numpy(x).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+
+
+def _draw_bf16(seed: int, tensor: int, shape, mult: Optional[float], pool) -> np.ndarray:
+    """The packed [rows, ...] tensor `tensor` of a workload, chunk by chunk from
+    independent streams, multiplied by `mult` in fp32, rounded to bf16."""
     out = np.empty(shape, dtype=np.uint16)
     rows = shape[0]
     per_row = int(np.prod(shape[1:]))
     m = None if mult is None else np.float32(mult)
-    for r0 in range(0, rows, chunk_rows):
-        n = min(chunk_rows, rows - r0)
-        x = rng.standard_normal(n * per_row, dtype=np.float32)
+
+    def chunk(c):
+        r0 = c * CHUNK_ROWS
+        n = min(CHUNK_ROWS, rows - r0)
+        g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([seed, tensor, c])))
+        x = g.standard_normal(n * per_row, dtype=np.float32)
         if m is not None:
             x *= m
-        out[r0:r0 + n] = f32_to_bf16_bits(x).reshape((n,) + tuple(shape[1:]))
+        out[r0:r0 + n] = _round_bf16(x).reshape((n,) + tuple(shape[1:]))
+
+    list(pool.map(chunk, range((rows + CHUNK_ROWS - 1) // CHUNK_ROWS)))
     return out
 
 
@@ -192,38 +210,34 @@ class GroupInputs:
     do_r: np.ndarray
 
 
-def make_inputs(shape: GroupShape, seed: int, rng: Optional[np.random.Generator] = None,
-                qk_mult: Optional[float] = None) -> GroupInputs:
+def make_inputs(shape: GroupShape, seed: int, qk_mult: Optional[float] = None, threads: Optional[int] = None) -> GroupInputs:
     """Draw the eight packed bf16 tensors. ``qk_mult`` overrides the 1/sqrt(d)
     multiplier of Q and K (V keeps 1/sqrt(d)); ``qk_mult=1.0`` gives the "sharp"
     inputs with logit std about 1."""
-    if rng is None:
-        rng = np.random.Generator(np.random.PCG64(seed))
+    import concurrent.futures as cf
+    import os
     hq, hkv, d = shape.num_q_heads, shape.num_kv_heads, shape.head_dim
     tp, tr = shape.total_prompt, shape.total_resp
     inv = 1.0 / math.sqrt(d)
     mq = inv if qk_mult is None else qk_mult
-    q_p = _draw_bf16(rng, (tp, hq, d), mq)
-    k_p = _draw_bf16(rng, (tp, hkv, d), mq)
-    v_p = _draw_bf16(rng, (tp, hkv, d), inv)
-    q_r = _draw_bf16(rng, (tr, hq, d), mq)
-    k_r = _draw_bf16(rng, (tr, hkv, d), mq)
-    v_r = _draw_bf16(rng, (tr, hkv, d), inv)
-    do_p = _draw_bf16(rng, (tp, hq, d), None)
-    do_r = _draw_bf16(rng, (tr, hq, d), None)
-    return GroupInputs(shape, q_p, k_p, v_p, q_r, k_r, v_r, do_p, do_r)
+    specs = [((tp, hq, d), mq), ((tp, hkv, d), mq), ((tp, hkv, d), inv),
+             ((tr, hq, d), mq), ((tr, hkv, d), mq), ((tr, hkv, d), inv),
+             ((tp, hq, d), None), ((tr, hq, d), None)]
+    import torch
+    n = threads or min(16, len(os.sched_getaffinity(0)))
+    prev = torch.get_num_threads()
+    torch.set_num_threads(1)  # parallelism comes from the chunk threads
+    try:
+        with cf.ThreadPoolExecutor(max_workers=n) as pool:
+            arrs = [_draw_bf16(seed, t, sh, mult, pool) for t, (sh, mult) in enumerate(specs)]
+    finally:
+        torch.set_num_threads(prev)
+    return GroupInputs(shape, *arrs)
 
 
 def make_config(name: str) -> GroupInputs:
-    """Shape and tensors of a named workload. For ``ragged`` the tensors continue
-    on the stream that drew the lengths."""
-    seed = CONFIG_SEEDS[name]
-    if name == "ragged":
-        rng = np.random.Generator(np.random.PCG64(seed))
-        ps, rs, _ = ragged_lengths(rng)
-        shape = GroupShape(ps, rs, 32, 8, 128)
-        return make_inputs(shape, seed, rng=rng)
-    return make_inputs(config_shape(name), seed)
+    """Shape and tensors of a named workload."""
+    return make_inputs(config_shape(name), CONFIG_SEEDS[name])
 
 
 def random_shape(rng: np.random.Generator, max_groups: int = 3, max_p: int = 300, max_g: int = 4,
