@@ -4,18 +4,21 @@
 //   dQ = s dS K,   dK = s dS^T Q,   dV = P^T dO.
 //
 // Two kernels, no atomics, every output written once:
-// * attn_dq_kernel (query-outer): one workgroup per 128-row query tile and
-//   query head, sweeping the same key segments as the forward (prompt keys,
-//   then the branch's own causal keys). S^T, dP^T and dS^T keep one query per
-//   lane; dQ^T += K^T dS^T takes dS^T straight from the accumulators and K^T
-//   by transpose reads of the row-major K tile.
-// * attn_dkv_kernel (key-outer): one workgroup per 128-key tile and KV head;
-//   each wavefront holds 32 keys (K and V rows in registers) and sweeps every
-//   query that sees them: the g query heads of the KV head (GQA) and, for
-//   prompt keys in replay, the response rows of every branch of the group, so
-//   the Eq. 2 sum over branches happens in the accumulators. Query tiles of 64
-//   rows are staged in LDS row-major; Q^T and dO^T operands come from
-//   transpose reads of the same tiles.
+// * attn_dq_kernel (query-outer): one workgroup (4 wavefronts, two workgroups
+//   per CU) per 128-row query tile and query head, sweeping the same key
+//   segments as the forward (prompt keys, then the branch's own causal keys)
+//   in 64-key blocks, each handled as two 32-key halves. S^T, dP^T and dS^T
+//   keep one query per lane; dQ^T += K^T dS^T takes dS^T straight from the
+//   accumulators and K^T by transpose reads of the row-major K tile.
+// * attn_dkv_kernel (key-outer): one workgroup (8 wavefronts, two per SIMD)
+//   per 128-key tile and KV head. Wavefronts w and w + 4 own the same 32 keys
+//   (K and V tiles in LDS) and take the two 32-row halves of
+//   every 64-row query block; their dK/dV partials are added through LDS at
+//   the end. The sweep covers every query that sees the keys: the g query
+//   heads of the KV head (GQA) and, for prompt keys in replay, the response
+//   rows of every branch of the group, so the Eq. 2 sum over branches happens
+//   in the accumulators. Query tiles are copied to LDS directly from global
+//   memory; Q^T and dO^T operands come from transpose reads.
 #include "common.h"
 #include "kernels.h"
 
@@ -29,15 +32,8 @@ constexpr int DQ_BM = 128;
 constexpr int DQ_BN = 64;
 
 template <int D>
-struct DqLds {
-  __bf16 k[2][DQ_BN * D];
-  __bf16 v[2][DQ_BN * D];
-};
-
-template <int D>
-__global__ __launch_bounds__(256, 1) void attn_dq_kernel(DqParams p) {
-  using L = DqLds<D>;
-  __shared__ L sm;
+__global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
+  __shared__ __bf16 k_buf0[DQ_BN * D], k_buf1[DQ_BN * D], v_buf0[DQ_BN * D], v_buf1[DQ_BN * D];
   int unit, hh;
   if (!xcd_unit(p.n_units, p.group, unit, hh)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
@@ -74,75 +70,71 @@ __global__ __launch_bounds__(256, 1) void attn_dq_kernel(DqParams p) {
   const int nB = (t.b_len + DQ_BN - 1) / DQ_BN;
   const int nblk = nA + nB;
 
-  TileStage<DQ_BN, D> kst, vst;
-  auto load_block = [&](int b) {
+  auto load_block = [&](int b, __bf16* kd, __bf16* vd) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * DQ_BN;
     const int len = isB ? t.b_len : t.a_len;
     const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
     const int nvalid = min(DQ_BN, len - kb0);
-    kst.load(isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
-    vst.load(isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
-  };
-  auto store_block = [&](int buf) {
-    kst.store(sm.k[buf]);
-    vst.store(sm.v[buf]);
+    tile_to_lds<DQ_BN, D, 4>(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
+    tile_to_lds<DQ_BN, D, 4>(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
 
-  if (nblk > 0) {
-    load_block(0);
-    store_block(0);
-  }
-  __syncthreads();
-
-  for (int b = 0; b < nblk; ++b) {
-    const int buf = b & 1;
-    if (b + 1 < nblk) load_block(b + 1);
+  auto compute = [&](int b, const __bf16* kl, const __bf16* vl) {
+    const int ol = opaque_lane();
+    const int orow = ol & 31, ohf = ol >> 5;
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * DQ_BN;
     const int len = isB ? t.b_len : t.a_len;
     const int qpos_lo = t.b_qpos + wave * 32;
-    const bool skip = isB && (kb0 > qpos_lo + 31);
-    if (!skip) {
-      f32x16 s0, s1, d0, d1;
+    const int qpos = t.b_qpos + qi;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; d0[i] = 0.f; d1[i] = 0.f; }
-      const __bf16* kl = sm.k[buf];
-      const __bf16* vl = sm.v[buf];
+    for (int half = 0; half < 2; ++half) {
+      const int k0 = kb0 + half * 32;  // first key of this 32-key half
+      const bool skip = isB && (k0 > qpos_lo + 31);
+      if (skip) continue;
+      f32x16 s, dp;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const int col = ks * 16 + hf * 8;
-        s0 = mfma32(lds_row8<D>(kl, l32, col), qreg[ks], s0);
-        s1 = mfma32(lds_row8<D>(kl, 32 + l32, col), qreg[ks], s1);
-        d0 = mfma32(lds_row8<D>(vl, l32, col), doreg[ks], d0);
-        d1 = mfma32(lds_row8<D>(vl, 32 + l32, col), doreg[ks], d1);
+        const int col = ks * 16 + ohf * 8;
+        s = mfma32(lds_row8<D>(kl, half * 32 + orow, col), qreg[ks], s);
+        dp = mfma32(lds_row8<D>(vl, half * 32 + orow, col), doreg[ks], dp);
       }
-      const bool need_mask = (kb0 + DQ_BN > len) || (isB && (kb0 + DQ_BN - 1 > qpos_lo));
-      const int qpos = t.b_qpos + qi;
+      const bool need_mask = (k0 + 32 > len) || (isB && (k0 + 31 > qpos_lo));
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        float a0 = s0[i] * c - lse2, a1 = s1[i] * c - lse2;
+        float a = s[i] * c - lse2;
         if (need_mask) {
-          const int k0 = kb0 + acc_row(i, hf), k1 = k0 + 32;
-          if ((k0 >= len) || (isB && k0 > qpos)) a0 = -INFINITY;
-          if ((k1 >= len) || (isB && k1 > qpos)) a1 = -INFINITY;
+          const int kk = k0 + acc_row(i, hf);
+          if ((kk >= len) || (isB && kk > qpos)) a = -INFINITY;
         }
-        const float p0 = __builtin_amdgcn_exp2f(a0), p1 = __builtin_amdgcn_exp2f(a1);
-        s0[i] = p0 * (d0[i] - dsq);
-        s1[i] = p1 * (d1[i] - dsq);
+        s[i] = __builtin_amdgcn_exp2f(a) * (dp[i] - dsq);
       }
-      const bf16x8 g0 = to_bf16x8(s0, 0), g1 = to_bf16x8(s0, 8);
-      const bf16x8 g2 = to_bf16x8(s1, 0), g3 = to_bf16x8(s1, 8);
+      const bf16x8 g0 = to_bf16x8(s, 0), g1 = to_bf16x8(s, 8);
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        acc[db] = mfma32(lds_tr_operand<D>(kl, 0, db * 32), g0, acc[db]);
-        acc[db] = mfma32(lds_tr_operand<D>(kl, 16, db * 32), g1, acc[db]);
-        acc[db] = mfma32(lds_tr_operand<D>(kl, 32, db * 32), g2, acc[db]);
-        acc[db] = mfma32(lds_tr_operand<D>(kl, 48, db * 32), g3, acc[db]);
+        acc[db] = mfma32(lds_tr_operand<D>(kl, half * 32, db * 32, ol), g0, acc[db]);
+        acc[db] = mfma32(lds_tr_operand<D>(kl, half * 32 + 16, db * 32, ol), g1, acc[db]);
       }
     }
-    if (b + 1 < nblk) store_block(buf ^ 1);
+  };
+
+  if (nblk > 0) load_block(0, k_buf0, v_buf0);
+  wait_vmem();
+  __syncthreads();
+  for (int b = 0; b < nblk; b += 2) {
+    if (b + 1 < nblk) load_block(b + 1, k_buf1, v_buf1);
+    compute(b, k_buf0, v_buf0);
+    wait_vmem();
     __syncthreads();
+    if (b + 1 < nblk) {
+      if (b + 2 < nblk) load_block(b + 2, k_buf0, v_buf0);
+      compute(b + 1, k_buf1, v_buf1);
+      wait_vmem();
+      __syncthreads();
+    }
   }
 
   if (qvalid) {
@@ -168,40 +160,31 @@ __global__ __launch_bounds__(256, 1) void attn_dq_kernel(DqParams p) {
 
 // ----------------------------------------------------------------------------- dK/dV
 
-constexpr int KV_BN = 128;  // keys per workgroup (32 per wavefront)
-constexpr int KV_BQ = 64;   // query rows per block
-
-template <int D>
-struct DkvLds {
-  __bf16 q[2][KV_BQ * D];
-  __bf16 dout[2][KV_BQ * D];
-  float lse2[2][KV_BQ];
-  float dsum[2][KV_BQ];
-};
+constexpr int KV_BN = 128;  // keys per workgroup (32 per wavefront pair)
+constexpr int KV_BQ = 64;   // query rows per block (32 per wavefront of a pair)
 
 template <int D, bool OUT32>
-__global__ __launch_bounds__(256, 1) void attn_dkv_kernel(DkvParams p) {
-  using L = DkvLds<D>;
-  __shared__ L sm;
+__global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
+  // the workgroup's K and V tiles (operands of S = Q K^T and dP = dO V^T);
+  // query blocks double-buffered in separate arrays; lse2 = LSE * log2(e),
+  // +inf past the end of the range
+  __shared__ __bf16 k_tile[KV_BN * D], v_tile[KV_BN * D];
+  __shared__ __bf16 q_buf0[KV_BQ * D], q_buf1[KV_BQ * D], o_buf0[KV_BQ * D], o_buf1[KV_BQ * D];
+  __shared__ float lse2_buf0[KV_BQ], lse2_buf1[KV_BQ], dsum_buf0[KV_BQ], dsum_buf1[KV_BQ];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
+  const int kq = wave & 3;   // 32-key slice of the tile
+  const int qs = wave >> 2;  // 32-row half of every query block
   const int tile_id = blockIdx.x / p.hkv;
   const int kvh = blockIdx.x - tile_id * p.hkv;
   const KVTile t = p.tiles[tile_id];
-  const int kw0 = wave * 32;
+  const int kw0 = kq * 32;
   const int kj = kw0 + l32;  // this lane's key (B-operand column)
   const bool kvalid = kj < t.kv_len;
   const int64_t qstride = (int64_t)p.hq * D;
   const int64_t kvstride = (int64_t)p.hkv * D;
 
-  bf16x8 kreg[D / 16], vreg[D / 16];
-  {
-    const int64_t off = ((int64_t)t.kv_row0 + kj) * kvstride + kvh * D + hf * 8;
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      kreg[ks] = as_bf16x8(kvalid ? ldg16(p.k + off + ks * 16) : make_uint4(0, 0, 0, 0));
-      vreg[ks] = as_bf16x8(kvalid ? ldg16(p.v + off + ks * 16) : make_uint4(0, 0, 0, 0));
-    }
-  }
+  tile_to_lds<KV_BN, D, 8>(k_tile, p.k, t.kv_row0, t.kv_len, kvstride, kvh * D);
+  tile_to_lds<KV_BN, D, 8>(v_tile, p.v, t.kv_row0, t.kv_len, kvstride, kvh * D);
   f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
@@ -212,83 +195,115 @@ __global__ __launch_bounds__(256, 1) void attn_dkv_kernel(DkvParams p) {
   const int nqb = (t.q_len + KV_BQ - 1) / KV_BQ;
   const int nblk = p.group * nqb;
 
-  TileStage<KV_BQ, D> qst, dost;
-  float stat = 0.f;  // lse2 (threads 0..63) or D (threads 64..127) of the staged block
-  auto load_block = [&](int b) {
+  float stat = 0.f;  // lse2 (threads 0..63) or D (threads 64..127) of the block being loaded
+  auto load_block = [&](int b, __bf16* qd, __bf16* od) {
     const int hh = kvh * p.group + b / nqb;
     const int qb = b % nqb;
     const int64_t row0 = (int64_t)t.q_row0 + qb * KV_BQ;
     const int nvalid = min(KV_BQ, t.q_len - qb * KV_BQ);
-    qst.load(p.q, row0, nvalid, qstride, hh * D);
-    dost.load(p.dout, row0, nvalid, qstride, hh * D);
+    tile_to_lds<KV_BQ, D, 8>(qd, p.q, row0, nvalid, qstride, hh * D);
+    tile_to_lds<KV_BQ, D, 8>(od, p.dout, row0, nvalid, qstride, hh * D);
     if (tid < KV_BQ)
       stat = tid < nvalid ? p.lse[(int64_t)hh * p.lse_rows + row0 + tid] * kLog2e : INFINITY;
     else if (tid < 2 * KV_BQ)
       stat = (tid - KV_BQ) < nvalid ? p.dsum[(int64_t)hh * p.lse_rows + row0 + tid - KV_BQ] : 0.f;
   };
-  auto store_block = [&](int buf) {
-    qst.store(sm.q[buf]);
-    dost.store(sm.dout[buf]);
-    if (tid < KV_BQ) sm.lse2[buf][tid] = stat;
-    else if (tid < 2 * KV_BQ) sm.dsum[buf][tid - KV_BQ] = stat;
+  auto store_stat = [&](float* ld, float* dd) {
+    if (tid < KV_BQ) ld[tid] = stat;
+    else if (tid < 2 * KV_BQ) dd[tid - KV_BQ] = stat;
+  };
+
+  const int key_pos = t.kpos0 + kj;  // this lane's key position (causal tiles)
+  auto compute = [&](int b, const __bf16* ql, const __bf16* dl, const float* lsel, const float* dsl) {
+    const int ol = opaque_lane();
+    const int orow = qs * 32 + (ol & 31), okey = kw0 + (ol & 31), ohf = ol >> 5;
+    const int qb = b % nqb;
+    const int qpos0 = t.qpos0 + qb * KV_BQ + qs * 32;  // position of this wave's first query
+    const bool skip = t.causal && (qpos0 + 31 < t.kpos0 + kw0);
+    if (skip) return;
+    const bool need_mask = t.causal && (qpos0 < t.kpos0 + kw0 + 31);
+    f32x16 s, dp;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) {
+      const int col = ks * 16 + ohf * 8;
+      s = mfma32(lds_row8<D>(ql, orow, col), lds_row8<D>(k_tile, okey, col), s);
+      dp = mfma32(lds_row8<D>(dl, orow, col), lds_row8<D>(v_tile, okey, col), dp);
+    }
+#pragma unroll
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const int r0 = qs * 32 + g4 * 8 + hf * 4;
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lsel[r0]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dsl[r0]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const int i = g4 * 4 + e;
+        float a = s[i] * c - l4[e];
+        if (need_mask && key_pos > qpos0 + g4 * 8 + hf * 4 + e) a = -INFINITY;
+        const float pr = __builtin_amdgcn_exp2f(a);
+        s[i] = pr;
+        dp[i] = pr * (dp[i] - d4[e]);
+      }
+    }
+    const bf16x8 pb0 = to_bf16x8(s, 0), pb1 = to_bf16x8(s, 8);
+    const bf16x8 gb0 = to_bf16x8(dp, 0), gb1 = to_bf16x8(dp, 8);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      dv[db] = mfma32(pb0, lds_tr_operand<D>(dl, qs * 32, db * 32, ol), dv[db]);
+      dv[db] = mfma32(pb1, lds_tr_operand<D>(dl, qs * 32 + 16, db * 32, ol), dv[db]);
+      dk[db] = mfma32(gb0, lds_tr_operand<D>(ql, qs * 32, db * 32, ol), dk[db]);
+      dk[db] = mfma32(gb1, lds_tr_operand<D>(ql, qs * 32 + 16, db * 32, ol), dk[db]);
+    }
   };
 
   if (nblk > 0) {
-    load_block(0);
-    store_block(0);
+    load_block(0, q_buf0, o_buf0);
+    store_stat(lse2_buf0, dsum_buf0);
   }
+  wait_vmem();
   __syncthreads();
-
-  for (int b = 0; b < nblk; ++b) {
-    const int buf = b & 1;
-    if (b + 1 < nblk) load_block(b + 1);
-    const int qb = b % nqb;
-    const int qblk_pos = t.qpos0 + qb * KV_BQ;       // position of the block's first query
-    const int key_pos = t.kpos0 + kj;               // this lane's key position
-    const bool skip = t.causal && (qblk_pos + KV_BQ - 1 < t.kpos0 + kw0);
-    if (!skip) {
-      const bool need_mask = t.causal && (qblk_pos < t.kpos0 + kw0 + 31);
-#pragma unroll
-      for (int qs = 0; qs < 2; ++qs) {
-        f32x16 s, dp;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
-        const __bf16* ql = sm.q[buf];
-        const __bf16* dl = sm.dout[buf];
-#pragma unroll
-        for (int ks = 0; ks < D / 16; ++ks) {
-          s = mfma32(lds_row8<D>(ql, qs * 32 + l32, ks * 16 + hf * 8), kreg[ks], s);
-          dp = mfma32(lds_row8<D>(dl, qs * 32 + l32, ks * 16 + hf * 8), vreg[ks], dp);
-        }
-#pragma unroll
-        for (int g4 = 0; g4 < 4; ++g4) {
-          const int r0 = qs * 32 + g4 * 8 + hf * 4;
-          const f32x4 l4 = *reinterpret_cast<const f32x4*>(&sm.lse2[buf][r0]);
-          const f32x4 d4 = *reinterpret_cast<const f32x4*>(&sm.dsum[buf][r0]);
-#pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            const int i = g4 * 4 + e;
-            float a = s[i] * c - l4[e];
-            if (need_mask && key_pos > qblk_pos + r0 + e) a = -INFINITY;
-            const float pr = __builtin_amdgcn_exp2f(a);
-            s[i] = pr;
-            dp[i] = pr * (dp[i] - d4[e]);
-          }
-        }
-        const bf16x8 pb0 = to_bf16x8(s, 0), pb1 = to_bf16x8(s, 8);
-        const bf16x8 gb0 = to_bf16x8(dp, 0), gb1 = to_bf16x8(dp, 8);
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db) {
-          dv[db] = mfma32(pb0, lds_tr_operand<D>(sm.dout[buf], qs * 32, db * 32), dv[db]);
-          dv[db] = mfma32(pb1, lds_tr_operand<D>(sm.dout[buf], qs * 32 + 16, db * 32), dv[db]);
-          dk[db] = mfma32(gb0, lds_tr_operand<D>(sm.q[buf], qs * 32, db * 32), dk[db]);
-          dk[db] = mfma32(gb1, lds_tr_operand<D>(sm.q[buf], qs * 32 + 16, db * 32), dk[db]);
-        }
-      }
+  for (int b = 0; b < nblk; b += 2) {
+    if (b + 1 < nblk) load_block(b + 1, q_buf1, o_buf1);
+    compute(b, q_buf0, o_buf0, lse2_buf0, dsum_buf0);
+    if (b + 1 < nblk) store_stat(lse2_buf1, dsum_buf1);
+    wait_vmem();
+    __syncthreads();
+    if (b + 1 < nblk) {
+      if (b + 2 < nblk) load_block(b + 2, q_buf0, o_buf0);
+      compute(b + 1, q_buf1, o_buf1, lse2_buf1, dsum_buf1);
+      if (b + 2 < nblk) store_stat(lse2_buf0, dsum_buf0);
+      wait_vmem();
+      __syncthreads();
     }
-    if (b + 1 < nblk) store_block(buf ^ 1);
+  }
+
+  // Add the partials of wavefronts w + 4 into w through LDS (the query-block
+  // buffers are free now; key slice kq uses one of the four), then wavefronts
+  // 0..3 write the tile. Accumulator register i of lane l sits at
+  // [db][i][lane] of the exchange buffer.
+  __bf16* xbuf = kq == 0 ? q_buf0 : kq == 1 ? q_buf1 : kq == 2 ? o_buf0 : o_buf1;
+  float* myx = reinterpret_cast<float*>(xbuf);
+  static_assert((D / 32) * 16 * 64 * 4 <= KV_BQ * D * 2, "exchange fits one query buffer");
+#pragma unroll
+  for (int round = 0; round < 2; ++round) {
+    f32x16* acc = round == 0 ? dk : dv;
+    if (qs == 1) {
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) myx[(db * 16 + i) * 64 + lane] = acc[db][i];
+    }
+    __syncthreads();
+    if (qs == 0) {
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) acc[db][i] += myx[(db * 16 + i) * 64 + lane];
+    }
     __syncthreads();
   }
+  if (qs != 0) return;
 
   // dK/dV tile: lane holds column d = 32*db + l32, rows = keys acc_row(i, hf)
 #pragma unroll
@@ -356,7 +371,7 @@ hipError_t launch_attn_dq(const DqParams& p0, int n_tiles, hipStream_t stream) {
 
 hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, bool out_f32, hipStream_t stream) {
   if (n_tiles == 0) return hipSuccess;
-  const dim3 grid((unsigned)n_tiles * (unsigned)p.hkv), block(256);
+  const dim3 grid((unsigned)n_tiles * (unsigned)p.hkv), block(512);
   if (p.head_dim == 128) {
     if (out_f32) hipLaunchKernelGGL((attn_dkv_kernel<128, true>), grid, block, 0, stream, p);
     else hipLaunchKernelGGL((attn_dkv_kernel<128, false>), grid, block, 0, stream, p);

@@ -14,7 +14,10 @@
 // output is rescaled only when a row maximum grows), and 16 MFMAs for
 // O^T += V^T P^T (V^T by transpose reads of the row-major V tile, P^T straight
 // from the S^T accumulators rounded to bf16). K and V tiles are
-// double-buffered in LDS and prefetched through registers one block ahead.
+// double-buffered in LDS (separate arrays, loop unrolled by two, so the
+// compiler can tell the buffer being filled from the one being read) and
+// copied there directly from global memory one block ahead
+// (global_load_lds), so no registers hold staged data.
 // The query heads of one KV head run on one XCD (shared K/V in its L2).
 #include "common.h"
 #include "kernels.h"
@@ -26,16 +29,9 @@ namespace {
 constexpr int BM = 128;  // query rows per workgroup
 constexpr int BN = 64;   // keys per block
 
-template <int D>
-struct FwdLds {
-  __bf16 k[2][BN * D];
-  __bf16 v[2][BN * D];
-};
-
 template <int D, bool OUT32>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
-  using L = FwdLds<D>;
-  __shared__ L sm;
+  __shared__ __bf16 k_buf0[BN * D], k_buf1[BN * D], v_buf0[BN * D], v_buf1[BN * D];
   int unit, hh;
   if (!xcd_unit(p.n_units, p.group, unit, hh)) return;
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
@@ -71,46 +67,33 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int nB = (t.b_len + BN - 1) / BN;
   const int nblk = nA + nB;
 
-  TileStage<BN, D> kst, vst;
-  auto load_block = [&](int b) {
+  auto load_block = [&](int b, __bf16* kd, __bf16* vd) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
     const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
     const int nvalid = min(BN, len - kb0);
-    kst.load(isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
-    vst.load(isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
-  };
-  auto store_block = [&](int buf) {
-    kst.store(sm.k[buf]);
-    vst.store(sm.v[buf]);
+    tile_to_lds<BN, D, 4>(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
+    tile_to_lds<BN, D, 4>(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
 
-  if (nblk > 0) {
-    load_block(0);
-    store_block(0);
-  }
-  __syncthreads();
-
-  for (int b = 0; b < nblk; ++b) {
-    const int buf = b & 1;
-    if (b + 1 < nblk) load_block(b + 1);
-
+  auto compute = [&](int b, const __bf16* kl, const __bf16* vl) {
+    const int ol = opaque_lane();
+    const int orow = ol & 31, ohf = ol >> 5;
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
     const int qpos_lo = t.b_qpos + wave * 32;  // causal: the wavefront's first query position
     const bool skip = isB && (kb0 > qpos_lo + 31);
     if (!skip) {
-      const __bf16* kl = sm.k[buf];
       f32x16 s0, s1;
 #pragma unroll
       for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const int col = ks * 16 + hf * 8;
-        s0 = mfma32(lds_row8<D>(kl, l32, col), qreg[ks], s0);
-        s1 = mfma32(lds_row8<D>(kl, 32 + l32, col), qreg[ks], s1);
+        const int col = ks * 16 + ohf * 8;
+        s0 = mfma32(lds_row8<D>(kl, orow, col), qreg[ks], s0);
+        s1 = mfma32(lds_row8<D>(kl, 32 + orow, col), qreg[ks], s1);
       }
       const bool need_mask = (kb0 + BN > len) || (isB && (kb0 + BN - 1 > qpos_lo));
       if (need_mask) {
@@ -149,17 +132,30 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       l_run += lsum;
       const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
       const bf16x8 pb2 = to_bf16x8(s1, 0), pb3 = to_bf16x8(s1, 8);
-      const __bf16* vl = sm.v[buf];
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        oacc[db] = mfma32(lds_tr_operand<D>(vl, 0, db * 32), pb0, oacc[db]);
-        oacc[db] = mfma32(lds_tr_operand<D>(vl, 16, db * 32), pb1, oacc[db]);
-        oacc[db] = mfma32(lds_tr_operand<D>(vl, 32, db * 32), pb2, oacc[db]);
-        oacc[db] = mfma32(lds_tr_operand<D>(vl, 48, db * 32), pb3, oacc[db]);
+        oacc[db] = mfma32(lds_tr_operand<D>(vl, 0, db * 32, ol), pb0, oacc[db]);
+        oacc[db] = mfma32(lds_tr_operand<D>(vl, 16, db * 32, ol), pb1, oacc[db]);
+        oacc[db] = mfma32(lds_tr_operand<D>(vl, 32, db * 32, ol), pb2, oacc[db]);
+        oacc[db] = mfma32(lds_tr_operand<D>(vl, 48, db * 32, ol), pb3, oacc[db]);
       }
     }
-    if (b + 1 < nblk) store_block(buf ^ 1);
+  };
+
+  if (nblk > 0) load_block(0, k_buf0, v_buf0);
+  wait_vmem();
+  __syncthreads();
+  for (int b = 0; b < nblk; b += 2) {
+    if (b + 1 < nblk) load_block(b + 1, k_buf1, v_buf1);
+    compute(b, k_buf0, v_buf0);
+    wait_vmem();
     __syncthreads();
+    if (b + 1 < nblk) {
+      if (b + 2 < nblk) load_block(b + 2, k_buf0, v_buf0);
+      compute(b + 1, k_buf1, v_buf1);
+      wait_vmem();
+      __syncthreads();
+    }
   }
 
   const float l_tot = l_run + __shfl_xor(l_run, 32);

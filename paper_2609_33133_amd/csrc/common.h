@@ -88,6 +88,15 @@ __device__ __forceinline__ bf16x8 lds_row8(const __bf16* tile, int row, int c) {
   return *reinterpret_cast<const bf16x8*>(tile + toff<D>(row, c));
 }
 
+// The lane index hidden from the optimiser: LDS addresses derived from it are
+// recomputed where they are used instead of being hoisted out of the block
+// loop and held in registers for the whole kernel.
+__device__ __forceinline__ int opaque_lane() {
+  int l = threadIdx.x & 63;
+  asm volatile("" : "+v"(l));
+  return l;
+}
+
 __device__ __forceinline__ s16x4 lds_tr16(const __bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
 }
@@ -99,8 +108,7 @@ __device__ __forceinline__ s16x4 lds_tr16(const __bf16* p) {
 // r0 = 16 s. Two ds_read_b64_tr_b16: inside each 16-lane group, lane j
 // addresses 4 columns of row (j / 4) and receives one column of 4 rows.
 template <int D>
-__device__ __forceinline__ bf16x8 lds_tr_operand(const __bf16* tile, int r0, int c0) {
-  const int lane = threadIdx.x & 63;
+__device__ __forceinline__ bf16x8 lds_tr_operand(const __bf16* tile, int r0, int c0, int lane) {
   const int grp = lane >> 4, j = lane & 15;
   const int col = c0 + 16 * (grp & 1) + 4 * (j & 3);
   const int row = r0 + 4 * (grp >> 1) + (j >> 2);
@@ -112,41 +120,32 @@ __device__ __forceinline__ bf16x8 lds_tr_operand(const __bf16* tile, int r0, int
   return r;
 }
 
-// Register-staged copy of a ROWS x D bf16 tile into a swizzled LDS tile. 256
-// threads; thread t owns rows (t / CH) * RPT .. +RPT-1 and chunk t % CH.
-template <int ROWS, int D>
-struct TileStage {
-  static constexpr int CH = D / 8;
-  static constexpr int RPT = ROWS * CH / 256;
-  static_assert(RPT >= 1, "rows per thread");
-  uint4 r[RPT];
-
-  // rows row0 .. row0+nvalid-1 of a [*, stride] bf16 tensor, column offset col0;
-  // rows past nvalid are zero
-  __device__ __forceinline__ void load(const uint16_t* base, int64_t row0, int nvalid, int64_t stride,
-                                       int col0) {
-    const int tid = threadIdx.x;
-    const int rg = tid / CH, dc = tid % CH;
+// Direct global -> LDS copy (global_load_lds_dwordx4) of a ROWS x D bf16 tile
+// into a swizzled LDS tile, by NWAVES wavefronts. One instruction writes 1 KB
+// of consecutive LDS bytes (lane L at +16 L) = RPI whole rows; lane L fills
+// physical chunk L % CH of row L / CH, so it loads logical chunk
+// (L % CH) ^ swz(row). Rows at or past nvalid (>= 1) read row nvalid - 1:
+// finite data that the caller masks. Completion: wait_vmem() then a barrier.
+template <int ROWS, int D, int NWAVES>
+__device__ __forceinline__ void tile_to_lds(__bf16* lds, const uint16_t* base, int64_t row0, int nvalid,
+                                            int64_t stride, int col0) {
+  constexpr int CH = D / 8, RPI = 64 / CH, NI = ROWS / RPI;
+  static_assert(ROWS % RPI == 0, "tile rows");
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int rsub = lane / CH, pc = lane % CH;
 #pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const int rr = rg * RPT + j;
-      if (rr < nvalid)
-        r[j] = ldg16(base + (row0 + rr) * stride + col0 + dc * 8);
-      else
-        r[j] = make_uint4(0, 0, 0, 0);
-    }
+  for (int i = wave; i < NI; i += NWAVES) {
+    const int row = i * RPI + rsub;
+    const int c = pc ^ swz<D>(row);
+    const int src = row < nvalid ? row : nvalid - 1;
+    const uint16_t* g = base + (row0 + src) * stride + col0 + c * 8;
+    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds + i * RPI * D), 16, 0, 0);
   }
+}
 
-  __device__ __forceinline__ void store(__bf16* lds) const {
-    const int tid = threadIdx.x;
-    const int rg = tid / CH, dc = tid % CH;
-#pragma unroll
-    for (int j = 0; j < RPT; ++j) {
-      const int row = rg * RPT + j;
-      *reinterpret_cast<uint4*>(lds + toff<D>(row, dc * 8)) = r[j];
-    }
-  }
-};
+// Wait for every outstanding vector-memory access of this wavefront
+// (s_waitcnt vmcnt(0)), e.g. direct-to-LDS copies before a barrier.
+__device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
 
 // ---------------------------------------------------------------------------- workgroup order
 
