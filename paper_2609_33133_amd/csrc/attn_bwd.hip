@@ -70,19 +70,20 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
   const int nB = (t.b_len + DQ_BN - 1) / DQ_BN;
   const int nblk = nA + nB;
 
+  TileCopy<DQ_BN, D, 4> cp;
+  cp.init(kvstride);
   auto load_block = [&](int b, __bf16* kd, __bf16* vd) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * DQ_BN;
     const int len = isB ? t.b_len : t.a_len;
     const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
     const int nvalid = min(DQ_BN, len - kb0);
-    tile_to_lds<DQ_BN, D, 4>(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
-    tile_to_lds<DQ_BN, D, 4>(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
+    cp.issue(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
+    cp.issue(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
 
   auto compute = [&](int b, const __bf16* kl, const __bf16* vl) {
-    const int ol = opaque_lane();
-    const int orow = ol & 31, ohf = ol >> 5;
+    const int ol = lane, orow = l32, ohf = hf;
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * DQ_BN;
     const int len = isB ? t.b_len : t.a_len;
@@ -183,8 +184,12 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   const int64_t qstride = (int64_t)p.hq * D;
   const int64_t kvstride = (int64_t)p.hkv * D;
 
-  tile_to_lds<KV_BN, D, 8>(k_tile, p.k, t.kv_row0, t.kv_len, kvstride, kvh * D);
-  tile_to_lds<KV_BN, D, 8>(v_tile, p.v, t.kv_row0, t.kv_len, kvstride, kvh * D);
+  {
+    TileCopy<KV_BN, D, 8> kc;
+    kc.init(kvstride);
+    kc.issue(k_tile, p.k, t.kv_row0, t.kv_len, kvstride, kvh * D);
+    kc.issue(v_tile, p.v, t.kv_row0, t.kv_len, kvstride, kvh * D);
+  }
   f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
   for (int db = 0; db < D / 32; ++db)
@@ -195,22 +200,31 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   const int nqb = (t.q_len + KV_BQ - 1) / KV_BQ;
   const int nblk = p.group * nqb;
 
-  float stat = 0.f;  // lse2 (threads 0..63) or D (threads 64..127) of the block being loaded
+  // Wavefront 0 loads the raw LSE and wavefront 1 the D values of the next
+  // query block into `stat`; they are scaled and stored to LDS at the end of
+  // the iteration, so nothing waits on these loads (or on the tile copies
+  // issued before them) while the current block is computed.
+  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
+  float stat = 0.f;
+  int stat_n = 0;
+  TileCopy<KV_BQ, D, 8> qc;
+  qc.init(qstride);
   auto load_block = [&](int b, __bf16* qd, __bf16* od) {
     const int hh = kvh * p.group + b / nqb;
     const int qb = b % nqb;
     const int64_t row0 = (int64_t)t.q_row0 + qb * KV_BQ;
     const int nvalid = min(KV_BQ, t.q_len - qb * KV_BQ);
-    tile_to_lds<KV_BQ, D, 8>(qd, p.q, row0, nvalid, qstride, hh * D);
-    tile_to_lds<KV_BQ, D, 8>(od, p.dout, row0, nvalid, qstride, hh * D);
-    if (tid < KV_BQ)
-      stat = tid < nvalid ? p.lse[(int64_t)hh * p.lse_rows + row0 + tid] * kLog2e : INFINITY;
-    else if (tid < 2 * KV_BQ)
-      stat = (tid - KV_BQ) < nvalid ? p.dsum[(int64_t)hh * p.lse_rows + row0 + tid - KV_BQ] : 0.f;
+    qc.issue(qd, p.q, row0, nvalid, qstride, hh * D);
+    qc.issue(od, p.dout, row0, nvalid, qstride, hh * D);
+    if (wave_u < 2) {
+      const float* src = (wave_u == 0 ? p.lse : p.dsum) + (int64_t)hh * p.lse_rows + row0;
+      stat = src[min(lane, nvalid - 1)];
+      stat_n = nvalid;
+    }
   };
   auto store_stat = [&](float* ld, float* dd) {
-    if (tid < KV_BQ) ld[tid] = stat;
-    else if (tid < 2 * KV_BQ) dd[tid - KV_BQ] = stat;
+    if (wave_u == 0) ld[lane] = lane < stat_n ? stat * kLog2e : INFINITY;
+    else if (wave_u == 1) dd[lane] = lane < stat_n ? stat : 0.f;
   };
 
   const int key_pos = t.kpos0 + kj;  // this lane's key position (causal tiles)

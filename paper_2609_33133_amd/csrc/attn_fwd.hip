@@ -67,19 +67,20 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int nB = (t.b_len + BN - 1) / BN;
   const int nblk = nA + nB;
 
+  TileCopy<BN, D, 4> cp;
+  cp.init(kvstride);
   auto load_block = [&](int b, __bf16* kd, __bf16* vd) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
     const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
     const int nvalid = min(BN, len - kb0);
-    tile_to_lds<BN, D, 4>(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
-    tile_to_lds<BN, D, 4>(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
+    cp.issue(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
+    cp.issue(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
 
   auto compute = [&](int b, const __bf16* kl, const __bf16* vl) {
-    const int ol = opaque_lane();
-    const int orow = ol & 31, ohf = ol >> 5;
+    const int ol = lane, orow = l32, ohf = hf;
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;

@@ -124,24 +124,46 @@ __device__ __forceinline__ bf16x8 lds_tr_operand(const __bf16* tile, int r0, int
 // into a swizzled LDS tile, by NWAVES wavefronts. One instruction writes 1 KB
 // of consecutive LDS bytes (lane L at +16 L) = RPI whole rows; lane L fills
 // physical chunk L % CH of row L / CH, so it loads logical chunk
-// (L % CH) ^ swz(row). Rows at or past nvalid (>= 1) read row nvalid - 1:
-// finite data that the caller masks. Completion: wait_vmem() then a barrier.
+// (L % CH) ^ swz(row). The per-lane source offsets do not depend on the block
+// and are computed once (TileCopy); a block adds its uniform base. Rows at or
+// past nvalid (>= 1) read row nvalid - 1: finite data that the caller masks.
+// Completion: wait_vmem() then a barrier.
 template <int ROWS, int D, int NWAVES>
-__device__ __forceinline__ void tile_to_lds(__bf16* lds, const uint16_t* base, int64_t row0, int nvalid,
-                                            int64_t stride, int col0) {
-  constexpr int CH = D / 8, RPI = 64 / CH, NI = ROWS / RPI;
+struct TileCopy {
+  static constexpr int CH = D / 8, RPI = 64 / CH, NI = ROWS / RPI;
+  static constexpr int PER_WAVE = (NI + NWAVES - 1) / NWAVES;
   static_assert(ROWS % RPI == 0, "tile rows");
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  const int rsub = lane / CH, pc = lane % CH;
+  int row[PER_WAVE];     // tile row this lane fills, per instruction of this wave
+  int off[PER_WAVE];     // its element offset inside a source row block (row * stride + chunk * 8)
+
+  __device__ __forceinline__ void init(int64_t stride) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
-  for (int i = wave; i < NI; i += NWAVES) {
-    const int row = i * RPI + rsub;
-    const int c = pc ^ swz<D>(row);
-    const int src = row < nvalid ? row : nvalid - 1;
-    const uint16_t* g = base + (row0 + src) * stride + col0 + c * 8;
-    __builtin_amdgcn_global_load_lds(g, (__attribute__((address_space(3))) void*)(lds + i * RPI * D), 16, 0, 0);
+    for (int k = 0; k < PER_WAVE; ++k) {
+      const int i = wave + k * NWAVES;
+      row[k] = i * RPI + lane / CH;
+      off[k] = (int)(row[k] * stride) + ((lane % CH) ^ swz<D>(row[k])) * 8;
+    }
   }
-}
+
+  // rows row0 .. row0 + nvalid - 1 of a [*, stride] tensor, columns col0 ..
+  __device__ __forceinline__ void issue(__bf16* lds, const uint16_t* base, int64_t row0, int nvalid, int64_t stride,
+                                        int col0) const {
+    const int wave = threadIdx.x >> 6;
+    const uint16_t* gb = base + row0 * stride + col0;
+    const bool full = nvalid >= ROWS;
+#pragma unroll
+    for (int k = 0; k < PER_WAVE; ++k) {
+      const int i = wave + k * NWAVES;
+      if (i < NI) {
+        int o = off[k];
+        if (!full && row[k] >= nvalid) o -= (row[k] - (nvalid - 1)) * (int)stride;
+        __builtin_amdgcn_global_load_lds(gb + o, (__attribute__((address_space(3))) void*)(lds + i * RPI * D), 16,
+                                         0, 0);
+      }
+    }
+  }
+};
 
 // Wait for every outstanding vector-memory access of this wavefront
 // (s_waitcnt vmcnt(0)), e.g. direct-to-LDS copies before a barrier.
