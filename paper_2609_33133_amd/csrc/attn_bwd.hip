@@ -209,9 +209,12 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   int stat_n = 0;
   TileCopy<KV_BQ, D, 8> qc;
   qc.init(qstride);
+  // query blocks are swept from the end of the range backwards, so that the
+  // concurrent causal tiles of one KV head (all ranges end at the segment end)
+  // read the same blocks at the same time and share them in L2
   auto load_block = [&](int b, __bf16* qd, __bf16* od) {
     const int hh = kvh * p.group + b / nqb;
-    const int qb = b % nqb;
+    const int qb = nqb - 1 - b % nqb;
     const int64_t row0 = (int64_t)t.q_row0 + qb * KV_BQ;
     const int nvalid = min(KV_BQ, t.q_len - qb * KV_BQ);
     qc.issue(qd, p.q, row0, nvalid, qstride, hh * D);
@@ -228,10 +231,13 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   };
 
   const int key_pos = t.kpos0 + kj;  // this lane's key position (causal tiles)
+  RowOffsets<D> qrow_off, key_off;   // Q/dO rows of this wave's half; K/V rows of its keys
+  qrow_off.init(qs * 32 + l32, hf);
+  key_off.init(kj, hf);
+  TrOffsets<D> qtr_off;              // Q^T / dO^T operands of this wave's half
+  qtr_off.init(qs * 32, lane);
   auto compute = [&](int b, const __bf16* ql, const __bf16* dl, const float* lsel, const float* dsl) {
-    const int ol = opaque_lane();
-    const int orow = qs * 32 + (ol & 31), okey = kw0 + (ol & 31), ohf = ol >> 5;
-    const int qb = b % nqb;
+    const int qb = nqb - 1 - b % nqb;
     const int qpos0 = t.qpos0 + qb * KV_BQ + qs * 32;  // position of this wave's first query
     const bool skip = t.causal && (qpos0 + 31 < t.kpos0 + kw0);
     if (skip) return;
@@ -241,9 +247,8 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      const int col = ks * 16 + ohf * 8;
-      s = mfma32(lds_row8<D>(ql, orow, col), lds_row8<D>(k_tile, okey, col), s);
-      dp = mfma32(lds_row8<D>(dl, orow, col), lds_row8<D>(v_tile, okey, col), dp);
+      s = mfma32(lds_row8_at<D>(ql, qrow_off.o[ks]), lds_row8_at<D>(k_tile, key_off.o[ks]), s);
+      dp = mfma32(lds_row8_at<D>(dl, qrow_off.o[ks]), lds_row8_at<D>(v_tile, key_off.o[ks]), dp);
     }
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
@@ -264,10 +269,10 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     const bf16x8 gb0 = to_bf16x8(dp, 0), gb1 = to_bf16x8(dp, 8);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
-      dv[db] = mfma32(pb0, lds_tr_operand<D>(dl, qs * 32, db * 32, ol), dv[db]);
-      dv[db] = mfma32(pb1, lds_tr_operand<D>(dl, qs * 32 + 16, db * 32, ol), dv[db]);
-      dk[db] = mfma32(gb0, lds_tr_operand<D>(ql, qs * 32, db * 32, ol), dk[db]);
-      dk[db] = mfma32(gb1, lds_tr_operand<D>(ql, qs * 32 + 16, db * 32, ol), dk[db]);
+      dv[db] = mfma32(pb0, qtr_off.read(dl, 0, db), dv[db]);
+      dv[db] = mfma32(pb1, qtr_off.read(dl, 1, db), dv[db]);
+      dk[db] = mfma32(gb0, qtr_off.read(ql, 0, db), dk[db]);
+      dk[db] = mfma32(gb1, qtr_off.read(ql, 1, db), dk[db]);
     }
   };
 

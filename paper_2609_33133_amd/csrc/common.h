@@ -97,6 +97,23 @@ __device__ __forceinline__ int opaque_lane() {
   return l;
 }
 
+// Per-lane byte offsets of the 16-byte row reads of a swizzled [*, D] tile:
+// row `row`, columns 16*ks + 8*hf .. +7 for ks = 0 .. D/16 - 1. A read is then
+// one ds_read_b128 at (offset register + tile base).
+template <int D>
+struct RowOffsets {
+  int o[D / 16];
+  __device__ __forceinline__ void init(int row, int hf) {
+#pragma unroll
+    for (int ks = 0; ks < D / 16; ++ks) o[ks] = 2 * toff<D>(row, ks * 16 + hf * 8);
+  }
+};
+
+template <int D>
+__device__ __forceinline__ bf16x8 lds_row8_at(const __bf16* tile, int byte_off) {
+  return *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(tile) + byte_off);
+}
+
 __device__ __forceinline__ s16x4 lds_tr16(const __bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
 }
@@ -119,6 +136,35 @@ __device__ __forceinline__ bf16x8 lds_tr_operand(const __bf16* tile, int r0, int
   __builtin_memcpy(reinterpret_cast<char*>(&r) + 8, &b, 8);
   return r;
 }
+
+// Per-lane byte offsets of the transposed operand reads (lds_tr_operand) of a
+// swizzled [*, D] tile for rows base_row + 16*m (+ 0..15) and columns
+// 32*db + (0..31): the swizzle depends on the row modulo 16 only, so 16*m rows
+// are a constant byte offset (16 * m * 2D) added to the table entry.
+template <int D>
+struct TrOffsets {
+  int o[D / 32][2];
+  __device__ __forceinline__ void init(int base_row, int lane) {
+    const int grp = lane >> 4, j = lane & 15;
+    const int row = base_row + 4 * (grp >> 1) + (j >> 2);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      const int col = 32 * db + 16 * (grp & 1) + 4 * (j & 3);
+      o[db][0] = 2 * toff<D>(row, col);
+      o[db][1] = 2 * toff<D>(row + 8, col);
+    }
+  }
+  // operand for rows base_row + 16*m .. and columns 32*db ..
+  __device__ __forceinline__ bf16x8 read(const __bf16* tile, int m, int db) const {
+    const char* t = reinterpret_cast<const char*>(tile) + m * 16 * D * 2;
+    const s16x4 a = lds_tr16(reinterpret_cast<const __bf16*>(t + o[db][0]));
+    const s16x4 b = lds_tr16(reinterpret_cast<const __bf16*>(t + o[db][1]));
+    bf16x8 r;
+    __builtin_memcpy(&r, &a, 8);
+    __builtin_memcpy(reinterpret_cast<char*>(&r) + 8, &b, 8);
+    return r;
+  }
+};
 
 // Direct global -> LDS copy (global_load_lds_dwordx4) of a ROWS x D bf16 tile
 // into a swizzled LDS tile, by NWAVES wavefronts. One instruction writes 1 KB
