@@ -82,8 +82,12 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
     cp.issue(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
 
+  RowOffsets<D> r0_off, r1_off;  // K/V rows l32 and 32 + l32
+  r0_off.init(l32, hf);
+  r1_off.init(32 + l32, hf);
+  TrOffsets<D> ktr_off;           // K^T operands
+  ktr_off.init(0, lane);
   auto compute = [&](int b, const __bf16* kl, const __bf16* vl) {
-    const int ol = lane, orow = l32, ohf = hf;
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * DQ_BN;
     const int len = isB ? t.b_len : t.a_len;
@@ -99,9 +103,9 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
       for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
-        const int col = ks * 16 + ohf * 8;
-        s = mfma32(lds_row8<D>(kl, half * 32 + orow, col), qreg[ks], s);
-        dp = mfma32(lds_row8<D>(vl, half * 32 + orow, col), doreg[ks], dp);
+        const int o = half ? r1_off.o[ks] : r0_off.o[ks];
+        s = mfma32(lds_row8_at<D>(kl, o), qreg[ks], s);
+        dp = mfma32(lds_row8_at<D>(vl, o), doreg[ks], dp);
       }
       const bool need_mask = (k0 + 32 > len) || (isB && (k0 + 31 > qpos_lo));
 #pragma unroll
@@ -116,8 +120,8 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
       const bf16x8 g0 = to_bf16x8(s, 0), g1 = to_bf16x8(s, 8);
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
-        acc[db] = mfma32(lds_tr_operand<D>(kl, half * 32, db * 32, ol), g0, acc[db]);
-        acc[db] = mfma32(lds_tr_operand<D>(kl, half * 32 + 16, db * 32, ol), g1, acc[db]);
+        acc[db] = mfma32(ktr_off.read(kl, 2 * half, db), g0, acc[db]);
+        acc[db] = mfma32(ktr_off.read(kl, 2 * half + 1, db), g1, acc[db]);
       }
     }
   };

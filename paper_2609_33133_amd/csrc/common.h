@@ -13,7 +13,7 @@
 // eight registers 8s..8s+7 of half-wave h cover rows 16s + 4h + {0..3} and
 // 16s + 8 + 4h + {0..3}, so the k index of that MFMA runs over those rows, and
 // the other operand is fetched from LDS in the same order with the gfx950
-// transpose read (lds_tr_operand).
+// transpose read (TrOffsets).
 //
 // LDS tiles are row-major, unpadded, with the 16-byte chunks of row r stored
 // at chunk index (chunk ^ swz(r)): 16-byte row reads of 16 consecutive rows
@@ -82,21 +82,6 @@ __device__ __forceinline__ int toff(int row, int col) {
   return row * D + ((((col >> 3) ^ swz<D>(row))) << 3) + (col & 7);
 }
 
-// 16-byte read of columns c .. c+7 (c % 8 == 0) of `row`
-template <int D>
-__device__ __forceinline__ bf16x8 lds_row8(const __bf16* tile, int row, int c) {
-  return *reinterpret_cast<const bf16x8*>(tile + toff<D>(row, c));
-}
-
-// The lane index hidden from the optimiser: LDS addresses derived from it are
-// recomputed where they are used instead of being hoisted out of the block
-// loop and held in registers for the whole kernel.
-__device__ __forceinline__ int opaque_lane() {
-  int l = threadIdx.x & 63;
-  asm volatile("" : "+v"(l));
-  return l;
-}
-
 // Per-lane byte offsets of the 16-byte row reads of a swizzled [*, D] tile:
 // row `row`, columns 16*ks + 8*hf .. +7 for ks = 0 .. D/16 - 1. A read is then
 // one ds_read_b128 at (offset register + tile base).
@@ -118,29 +103,15 @@ __device__ __forceinline__ s16x4 lds_tr16(const __bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
 }
 
-// MFMA operand whose k index runs along the rows of a swizzled tile: lane l
-// gets column c0 + (l % 32) at rows r0 + 4*(l/32) + {0,1,2,3} (elements 0..3)
-// and r0 + 8 + 4*(l/32) + {0,1,2,3} (elements 4..7), i.e. exactly the rows
-// that accumulator registers 8s..8s+7 of the same half-wave hold when
-// r0 = 16 s. Two ds_read_b64_tr_b16: inside each 16-lane group, lane j
-// addresses 4 columns of row (j / 4) and receives one column of 4 rows.
-template <int D>
-__device__ __forceinline__ bf16x8 lds_tr_operand(const __bf16* tile, int r0, int c0, int lane) {
-  const int grp = lane >> 4, j = lane & 15;
-  const int col = c0 + 16 * (grp & 1) + 4 * (j & 3);
-  const int row = r0 + 4 * (grp >> 1) + (j >> 2);
-  const s16x4 a = lds_tr16(tile + toff<D>(row, col));
-  const s16x4 b = lds_tr16(tile + toff<D>(row + 8, col));
-  bf16x8 r;
-  __builtin_memcpy(&r, &a, 8);
-  __builtin_memcpy(reinterpret_cast<char*>(&r) + 8, &b, 8);
-  return r;
-}
-
-// Per-lane byte offsets of the transposed operand reads (lds_tr_operand) of a
-// swizzled [*, D] tile for rows base_row + 16*m (+ 0..15) and columns
-// 32*db + (0..31): the swizzle depends on the row modulo 16 only, so 16*m rows
-// are a constant byte offset (16 * m * 2D) added to the table entry.
+// MFMA operand whose k index runs along the rows of a swizzled tile (transpose
+// reads): lane l gets column c0 + (l % 32) at rows r0 + 4*(l/32) + {0,1,2,3}
+// (elements 0..3) and r0 + 8 + 4*(l/32) + {0,1,2,3} (elements 4..7), i.e.
+// exactly the rows that accumulator registers 8s..8s+7 of the same half-wave
+// hold when r0 = 16 s. Two ds_read_b64_tr_b16: inside each 16-lane group,
+// lane j addresses 4 columns of row (j / 4) and receives one column of 4 rows.
+// TrOffsets holds the per-lane byte offsets for rows base_row + 16*m
+// (+ 0..15) and columns c0 = 32*db: the swizzle depends on the row modulo 16
+// only, so 16*m rows are a constant byte offset (16 * m * 2D).
 template <int D>
 struct TrOffsets {
   int o[D / 32][2];
