@@ -57,8 +57,22 @@ def build(verbose: bool = False) -> str:
         list(ex.map(lambda j: _run(j[0], verbose), jobs))
     tmp = OUT + ".tmp"
     _run([cc, "--offload-arch=" + ARCH, "-shared", "-fPIC", "-o", tmp, *[o for _, o in jobs]], verbose)
+    _check_kernel_stubs(tmp)
     os.replace(tmp, OUT)
     return OUT
+
+
+def _check_kernel_stubs(lib: str) -> None:
+    """Every kernel launch stub must be defined in the library: an undefined one
+    would only fail when the library is loaded."""
+    nm = shutil.which("nm") or "/usr/bin/nm"
+    r = subprocess.run([nm, "-D", "--undefined-only", lib], capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError("nm failed on " + lib + ":\n" + r.stderr)
+    missing = [ln.split()[-1] for ln in r.stdout.splitlines() if "__device_stub__" in ln]
+    if missing:
+        os.remove(lib)
+        raise RuntimeError("kernel launch stubs missing from the library: " + ", ".join(missing))
 
 
 if __name__ == "__main__":

@@ -30,6 +30,7 @@ namespace {
 
 constexpr int DQ_BM = 128;
 constexpr int DQ_BN = 64;
+constexpr int DQ_DEPTH = 4;  // LDS operand reads run this many MFMAs ahead
 
 template <int D>
 __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
@@ -107,6 +108,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
         s = mfma32(lds_row8_at<D>(kl, o), qreg[ks], s);
         dp = mfma32(lds_row8_at<D>(vl, o), doreg[ks], dp);
       }
+      pace_lds_mfma<D / 8, 1, DQ_DEPTH>();
       const bool need_mask = (k0 + 32 > len) || (isB && (k0 + 31 > qpos_lo));
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
@@ -123,6 +125,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
         acc[db] = mfma32(ktr_off.read(kl, 2 * half, db), g0, acc[db]);
         acc[db] = mfma32(ktr_off.read(kl, 2 * half + 1, db), g1, acc[db]);
       }
+      pace_lds_mfma<D / 16, 2, DQ_DEPTH>();
     }
   };
 
@@ -167,6 +170,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 
 constexpr int KV_BN = 128;  // keys per workgroup (32 per wavefront pair)
 constexpr int KV_BQ = 64;   // query rows per block (32 per wavefront of a pair)
+constexpr int DKV_DEPTH = 2;  // LDS operand reads run this many MFMAs ahead
 
 template <int D, bool OUT32>
 __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
@@ -213,12 +217,14 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   int stat_n = 0;
   TileCopy<KV_BQ, D, 8> qc;
   qc.init(qstride);
-  // query blocks are swept from the end of the range backwards, so that the
-  // concurrent causal tiles of one KV head (all ranges end at the segment end)
-  // read the same blocks at the same time and share them in L2
+  // Block b is query block nqb - 1 - b / group of query head b % group: the
+  // query blocks are swept from the end of the range backwards and the g
+  // heads of a block are taken one after the other, so that the concurrent
+  // tiles of one KV head (causal ranges all end at the segment end) stay at
+  // the same query rows and share the Q / dO blocks in L2.
   auto load_block = [&](int b, __bf16* qd, __bf16* od) {
-    const int hh = kvh * p.group + b / nqb;
-    const int qb = nqb - 1 - b % nqb;
+    const int hh = kvh * p.group + b % p.group;
+    const int qb = nqb - 1 - b / p.group;
     const int64_t row0 = (int64_t)t.q_row0 + qb * KV_BQ;
     const int nvalid = min(KV_BQ, t.q_len - qb * KV_BQ);
     qc.issue(qd, p.q, row0, nvalid, qstride, hh * D);
@@ -241,7 +247,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   TrOffsets<D> qtr_off;              // Q^T / dO^T operands of this wave's half
   qtr_off.init(qs * 32, lane);
   auto compute = [&](int b, const __bf16* ql, const __bf16* dl, const float* lsel, const float* dsl) {
-    const int qb = nqb - 1 - b % nqb;
+    const int qb = nqb - 1 - b / p.group;
     const int qpos0 = t.qpos0 + qb * KV_BQ + qs * 32;  // position of this wave's first query
     const bool skip = t.causal && (qpos0 + 31 < t.kpos0 + kw0);
     if (skip) return;
@@ -254,6 +260,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
       s = mfma32(lds_row8_at<D>(ql, qrow_off.o[ks]), lds_row8_at<D>(k_tile, key_off.o[ks]), s);
       dp = mfma32(lds_row8_at<D>(dl, qrow_off.o[ks]), lds_row8_at<D>(v_tile, key_off.o[ks]), dp);
     }
+    pace_lds_mfma<D / 8, 2, DKV_DEPTH>();
 #pragma unroll
     for (int g4 = 0; g4 < 4; ++g4) {
       const int r0 = qs * 32 + g4 * 8 + hf * 4;
@@ -278,6 +285,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
       dk[db] = mfma32(gb0, qtr_off.read(ql, 0, db), dk[db]);
       dk[db] = mfma32(gb1, qtr_off.read(ql, 1, db), dk[db]);
     }
+    pace_lds_mfma<D / 8, 2, DKV_DEPTH>();
   };
 
   if (nblk > 0) {

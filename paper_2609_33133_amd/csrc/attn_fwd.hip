@@ -13,14 +13,11 @@
 // Q^T held in registers), the online-softmax update in fp32 with exp2 (the
 // output is rescaled only when a row maximum grows), and 16 MFMAs for
 // O^T += V^T P^T (V^T by transpose reads of the row-major V tile, P^T straight
-// from the S^T accumulators rounded to bf16). The S^T MFMAs of the next block
-// are issued between the max and the exponentials of the current one, so a
-// wavefront has matrix and vector work in flight together. K and V tiles are
+// from the S^T accumulators rounded to bf16). K and V tiles are
 // double-buffered in LDS (separate arrays, loop unrolled by two, so the
 // compiler can tell the buffer being filled from the one being read) and
-// copied there directly from global memory (global_load_lds), so no
-// registers hold staged data; LDS addresses come from per-lane offset tables
-// computed once.
+// copied there directly from global memory one block ahead
+// (global_load_lds), so no registers hold staged data.
 // The query heads of one KV head run on one XCD (shared K/V in its L2).
 #include "common.h"
 #include "kernels.h"
@@ -31,6 +28,7 @@ namespace {
 
 constexpr int BM = 128;  // query rows per workgroup
 constexpr int BN = 64;   // keys per block
+constexpr int FWD_DEPTH = 4;  // LDS operand reads run this many MFMAs ahead
 
 template <int D, bool OUT32>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
@@ -72,125 +70,95 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
   TileCopy<BN, D, 4> cp;
   cp.init(kvstride);
-  auto block_src = [&](int b, const uint16_t* a_src, const uint16_t* b_src, const uint16_t*& src, int64_t& row0,
-                       int& nvalid) {
+  auto load_block = [&](int b, __bf16* kd, __bf16* vd) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
-    src = isB ? b_src : a_src;
-    row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
-    nvalid = min(BN, len - kb0);
-  };
-  auto load_k = [&](int b, __bf16* kd) {
-    const uint16_t* src;
-    int64_t row0;
-    int nvalid;
-    block_src(b, p.ka, p.kb, src, row0, nvalid);
-    cp.issue(kd, src, row0, nvalid, kvstride, kvh * D);
-  };
-  auto load_v = [&](int b, __bf16* vd) {
-    const uint16_t* src;
-    int64_t row0;
-    int nvalid;
-    block_src(b, p.va, p.vb, src, row0, nvalid);
-    cp.issue(vd, src, row0, nvalid, kvstride, kvh * D);
+    const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
+    const int nvalid = min(BN, len - kb0);
+    cp.issue(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
+    cp.issue(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
 
-  RowOffsets<D> k0_off, k1_off;  // K rows l32 and 32 + l32
-  k0_off.init(l32, hf);
-  k1_off.init(32 + l32, hf);
-  TrOffsets<D> vtr_off;           // V^T operands
+  RowOffsets<D> k_off;  // K row l32; row 32 + l32 has the same swizzle, 32 rows further
+  k_off.init(l32, hf);
+  TrOffsets<D> vtr_off;  // V^T operands
   vtr_off.init(0, lane);
-
-  // S^T of one 64-key block: two 32-key halves
-  auto s_mfma = [&](const __bf16* kl, f32x16& s0, f32x16& s1) {
-#pragma unroll
-    for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; }
-#pragma unroll
-    for (int ks = 0; ks < D / 16; ++ks) {
-      s0 = mfma32(lds_row8_at<D>(kl, k0_off.o[ks]), qreg[ks], s0);
-      s1 = mfma32(lds_row8_at<D>(kl, k1_off.o[ks]), qreg[ks], s1);
-    }
-  };
-
-  // Softmax and P V of block b (scores in s0/s1). The S^T MFMAs of block
-  // b + 1 (into n0/n1, from kl_next) are issued in the same branch-free region
-  // as the exponentials of block b, so the matrix cores and the vector ALUs of
-  // this wavefront work at the same time. On the last block the extra S^T is
-  // computed from a stale buffer and never used.
-  auto step = [&](int b, f32x16& s0, f32x16& s1, const __bf16* vl, const __bf16* kl_next, f32x16& n0,
-                  f32x16& n1) {
+  auto compute = [&](int b, const __bf16* kl, const __bf16* vl) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
     const int qpos_lo = t.b_qpos + wave * 32;  // causal: the wavefront's first query position
-    const bool need_mask = (kb0 + BN > len) || (isB && (kb0 + BN - 1 > qpos_lo));
-    if (need_mask) {
-      const int lim = min(len - 1, isB ? t.b_qpos + qi : len - 1) - kb0;  // last visible key of the block
+    const bool skip = isB && (kb0 > qpos_lo + 31);
+    if (!skip) {
+      f32x16 s0, s1;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; }
+#pragma unroll
+      for (int ks = 0; ks < D / 16; ++ks) {
+        s0 = mfma32(lds_row8_at<D>(kl, k_off.o[ks]), qreg[ks], s0);
+        s1 = mfma32(lds_row8_at<D>(kl + 32 * D, k_off.o[ks]), qreg[ks], s1);
+      }
+      pace_lds_mfma<D / 8, 1, FWD_DEPTH>();
+      const bool need_mask = (kb0 + BN > len) || (isB && (kb0 + BN - 1 > qpos_lo));
+      if (need_mask) {
+        const int qpos = t.b_qpos + qi;
+#pragma unroll
+        for (int i = 0; i < 16; ++i) {
+          const int k0 = kb0 + acc_row(i, hf);
+          const int k1 = k0 + 32;
+          if ((k0 >= len) || (isB && k0 > qpos)) s0[i] = -INFINITY;
+          if ((k1 >= len) || (isB && k1 > qpos)) s1[i] = -INFINITY;
+        }
+      }
+      float mx = -INFINITY;
+#pragma unroll
+      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
+      mx = fmaxf(mx, __shfl_xor(mx, 32));
+      const float mnew = fmaxf(m_run, mx);
+      if (__any(mnew > m_run)) {
+        // rescale only when some row maximum of this wavefront grew
+        const float alpha = (mnew == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run - mnew) * c);
+        l_run *= alpha;
+#pragma unroll
+        for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+          for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+        m_run = mnew;
+      }
+      const float ms = (m_run == -INFINITY) ? 0.f : m_run * c;
+      float lsum = 0.f;
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        if (acc_row(i, hf) > lim) s0[i] = -INFINITY;
-        if (acc_row(i, hf) + 32 > lim) s1[i] = -INFINITY;
+        s0[i] = __builtin_amdgcn_exp2f(s0[i] * c - ms);
+        s1[i] = __builtin_amdgcn_exp2f(s1[i] * c - ms);
+        lsum += s0[i] + s1[i];
       }
-    }
-    float mx = -INFINITY;
+      l_run += lsum;
+      const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
+      const bf16x8 pb2 = to_bf16x8(s1, 0), pb3 = to_bf16x8(s1, 8);
 #pragma unroll
-    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
-    const float mnew = fmaxf(m_run, mx);
-    if (__any(mnew > m_run)) {
-      // rescale only when some row maximum of this wavefront grew
-      const float alpha = (mnew == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run - mnew) * c);
-      l_run *= alpha;
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-      m_run = mnew;
-    }
-    const float ms = (m_run == -INFINITY) ? 0.f : m_run * c;
-    s_mfma(kl_next, n0, n1);
-    float lsum = 0.f;
-#pragma unroll
-    for (int i = 0; i < 16; ++i) {
-      s0[i] = __builtin_amdgcn_exp2f(s0[i] * c - ms);
-      s1[i] = __builtin_amdgcn_exp2f(s1[i] * c - ms);
-      lsum += s0[i] + s1[i];
-    }
-    l_run += lsum;
-    const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
-    const bf16x8 pb2 = to_bf16x8(s1, 0), pb3 = to_bf16x8(s1, 8);
-#pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-      oacc[db] = mfma32(vtr_off.read(vl, 0, db), pb0, oacc[db]);
-      oacc[db] = mfma32(vtr_off.read(vl, 1, db), pb1, oacc[db]);
-      oacc[db] = mfma32(vtr_off.read(vl, 2, db), pb2, oacc[db]);
-      oacc[db] = mfma32(vtr_off.read(vl, 3, db), pb3, oacc[db]);
+      for (int db = 0; db < D / 32; ++db) {
+        oacc[db] = mfma32(vtr_off.read(vl, 0, db), pb0, oacc[db]);
+        oacc[db] = mfma32(vtr_off.read(vl, 1, db), pb1, oacc[db]);
+        oacc[db] = mfma32(vtr_off.read(vl, 2, db), pb2, oacc[db]);
+        oacc[db] = mfma32(vtr_off.read(vl, 3, db), pb3, oacc[db]);
+      }
+      pace_lds_mfma<D / 8, 2, FWD_DEPTH>();
     }
   };
 
-  // K(b + 1) and V(b) are resident while block b is processed; iteration b
-  // loads K(b + 2) over K(b) and V(b + 1) over V(b - 1).
-  f32x16 sa0, sa1, sb0, sb1;
-  if (nblk > 0) {
-    load_k(0, k_buf0);
-    load_v(0, v_buf0);
-    if (nblk > 1) load_k(1, k_buf1);
-  }
+  if (nblk > 0) load_block(0, k_buf0, v_buf0);
   wait_vmem();
   __syncthreads();
-  s_mfma(k_buf0, sa0, sa1);
-  __syncthreads();
   for (int b = 0; b < nblk; b += 2) {
-    if (b + 2 < nblk) load_k(b + 2, k_buf0);
-    if (b + 1 < nblk) load_v(b + 1, v_buf1);
-    step(b, sa0, sa1, v_buf0, k_buf1, sb0, sb1);
+    if (b + 1 < nblk) load_block(b + 1, k_buf1, v_buf1);
+    compute(b, k_buf0, v_buf0);
     wait_vmem();
     __syncthreads();
     if (b + 1 < nblk) {
-      if (b + 3 < nblk) load_k(b + 3, k_buf1);
-      if (b + 2 < nblk) load_v(b + 2, v_buf0);
-      step(b + 1, sb0, sb1, v_buf1, k_buf0, sa0, sa1);
+      if (b + 2 < nblk) load_block(b + 2, k_buf0, v_buf0);
+      compute(b + 1, k_buf1, v_buf1);
       wait_vmem();
       __syncthreads();
     }

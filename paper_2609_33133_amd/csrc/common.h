@@ -137,54 +137,76 @@ struct TrOffsets {
   }
 };
 
-// Direct global -> LDS copy (global_load_lds_dwordx4) of a ROWS x D bf16 tile
-// into a swizzled LDS tile, by NWAVES wavefronts. One instruction writes 1 KB
-// of consecutive LDS bytes (lane L at +16 L) = RPI whole rows; lane L fills
-// physical chunk L % CH of row L / CH, so it loads logical chunk
-// (L % CH) ^ swz(row). The per-lane source offsets do not depend on the block
-// and are computed once (TileCopy); a block adds its uniform base. Rows at or
-// past nvalid (>= 1) read row nvalid - 1: finite data that the caller masks.
+// Direct global -> LDS copy (buffer_load_dwordx4 ... lds) of a ROWS x D bf16
+// tile into a swizzled LDS tile, by NWAVES wavefronts. One instruction writes
+// 1 KB of consecutive LDS bytes (lane L at +16 L) = RPI whole rows; lane L
+// fills physical chunk L % CH of row L / CH, so it loads logical chunk
+// (L % CH) ^ swz(row). The per-lane source byte offsets do not depend on the
+// block and are computed once; a block builds a buffer descriptor at its
+// (uniform) first row whose range ends after row nvalid - 1, so rows past the
+// end read as zeros. The buffer form (not the global form) matters: the
+// compiler tracks it on the vector-memory counter only, so LDS reads issued
+// while a copy is in flight can still be waited for one at a time.
 // Completion: wait_vmem() then a barrier.
 template <int ROWS, int D, int NWAVES>
 struct TileCopy {
   static constexpr int CH = D / 8, RPI = 64 / CH, NI = ROWS / RPI;
   static constexpr int PER_WAVE = (NI + NWAVES - 1) / NWAVES;
   static_assert(ROWS % RPI == 0, "tile rows");
-  int row[PER_WAVE];     // tile row this lane fills, per instruction of this wave
-  int off[PER_WAVE];     // its element offset inside a source row block (row * stride + chunk * 8)
+  uint32_t off[PER_WAVE];  // byte offset of this lane's chunk inside a block of rows
 
   __device__ __forceinline__ void init(int64_t stride) {
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
 #pragma unroll
     for (int k = 0; k < PER_WAVE; ++k) {
       const int i = wave + k * NWAVES;
-      row[k] = i * RPI + lane / CH;
-      off[k] = (int)(row[k] * stride) + ((lane % CH) ^ swz<D>(row[k])) * 8;
+      const int row = i * RPI + lane / CH;
+      off[k] = 2u * (uint32_t)(row * stride + ((lane % CH) ^ swz<D>(row)) * 8);
     }
   }
 
-  // rows row0 .. row0 + nvalid - 1 of a [*, stride] tensor, columns col0 ..
+  // rows row0 .. row0 + nvalid - 1 (1 <= nvalid) of a [*, stride] tensor,
+  // columns col0 .. col0 + D - 1; tile rows from nvalid on are zero
   __device__ __forceinline__ void issue(__bf16* lds, const uint16_t* base, int64_t row0, int nvalid, int64_t stride,
                                         int col0) const {
-    const int wave = threadIdx.x >> 6;
+    // Device pass only: with a buffer-resource value in a kernel body, the
+    // host pass silently drops the launch stubs of some instantiations.
+#if defined(__HIP_DEVICE_COMPILE__)
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const uint16_t* gb = base + row0 * stride + col0;
-    const bool full = nvalid >= ROWS;
+    const int rows = nvalid < ROWS ? nvalid : ROWS;
+    const __amdgpu_buffer_rsrc_t rsrc =
+        __builtin_amdgcn_make_buffer_rsrc((void*)gb, 0, (int)(rows * stride * 2), 0x00020000);
 #pragma unroll
     for (int k = 0; k < PER_WAVE; ++k) {
       const int i = wave + k * NWAVES;
-      if (i < NI) {
-        int o = off[k];
-        if (!full && row[k] >= nvalid) o -= (row[k] - (nvalid - 1)) * (int)stride;
-        __builtin_amdgcn_global_load_lds(gb + o, (__attribute__((address_space(3))) void*)(lds + i * RPI * D), 16,
-                                         0, 0);
-      }
+      if (i < NI)
+        __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(lds + i * RPI * D),
+                                                 16, off[k], 0, 0, 0);
     }
+#endif
   }
 };
 
 // Wait for every outstanding vector-memory access of this wavefront
 // (s_waitcnt vmcnt(0)), e.g. direct-to-LDS copies before a barrier.
 __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70); }
+
+// Scheduling of a run of N MFMAs that take R LDS reads each: the reads are
+// issued DEPTH MFMAs ahead of the MFMA that consumes them, so the LDS latency
+// is covered by matrix work instead of a wait in front of every MFMA. Placed
+// after the run, in the same basic block; costs R * DEPTH operand registers.
+template <int N, int R, int DEPTH>
+__device__ __forceinline__ void pace_lds_mfma() {
+  static_assert(DEPTH >= 1 && DEPTH <= N, "prefetch depth");
+  __builtin_amdgcn_sched_group_barrier(0x100, R * DEPTH, 0);  // DS reads
+#pragma unroll
+  for (int i = 0; i < N - DEPTH; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);        // DS reads
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, DEPTH, 0);
+}
 
 // ---------------------------------------------------------------------------- workgroup order
 
