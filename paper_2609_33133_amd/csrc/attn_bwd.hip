@@ -170,7 +170,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 
 constexpr int KV_BN = 128;  // keys per workgroup (32 per wavefront pair)
 constexpr int KV_BQ = 64;   // query rows per block (32 per wavefront of a pair)
-constexpr int DKV_DEPTH = 2;  // LDS operand reads run this many MFMAs ahead
+constexpr int DKV_DEPTH = 3;  // LDS operand reads run this many MFMAs ahead
 
 template <int D, bool OUT32>
 __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {

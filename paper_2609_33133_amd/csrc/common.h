@@ -198,14 +198,15 @@ __device__ __forceinline__ void wait_vmem() { __builtin_amdgcn_s_waitcnt(0x0F70)
 // after the run, in the same basic block; costs R * DEPTH operand registers.
 template <int N, int R, int DEPTH>
 __device__ __forceinline__ void pace_lds_mfma() {
-  static_assert(DEPTH >= 1 && DEPTH <= N, "prefetch depth");
-  __builtin_amdgcn_sched_group_barrier(0x100, R * DEPTH, 0);  // DS reads
+  static_assert(DEPTH >= 1, "prefetch depth");
+  constexpr int DP = DEPTH < N ? DEPTH : N;
+  __builtin_amdgcn_sched_group_barrier(0x100, R * DP, 0);  // DS reads
 #pragma unroll
-  for (int i = 0; i < N - DEPTH; ++i) {
-    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);        // MFMA
-    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);        // DS reads
+  for (int i = 0; i < N - DP; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);     // MFMA
+    __builtin_amdgcn_sched_group_barrier(0x100, R, 0);     // DS reads
   }
-  __builtin_amdgcn_sched_group_barrier(0x008, DEPTH, 0);
+  __builtin_amdgcn_sched_group_barrier(0x008, DP, 0);
 }
 
 // ---------------------------------------------------------------------------- workgroup order
