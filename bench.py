@@ -19,10 +19,14 @@ of the same workload (cpu_baseline).
 from __future__ import annotations
 
 import argparse
+import csv
 import ctypes
+import glob
+import hashlib
 import json
 import math
 import os
+import re
 import sys
 import time
 
@@ -82,6 +86,119 @@ def role_work(role: str, shape, n_seed: int):
     if role == "lse_merge":
         return "byte", float(tr * hq * (2 * d * 4 + 2 * 4 + d * 2 + 4))
     raise KeyError(role)
+
+
+# profiles/ file names per workload
+WORKLOAD_SLUG = {"tiny": "tiny_P256_G2", "balanced": "balanced_4groups_P4096_G8", "prompt": "prompt_P32768_G8",
+                 "response": "response_P2048_G16", "ragged": "ragged_16groups"}
+
+
+def kernel_source_hash() -> str:
+    """Hash of every native source the kernels and their schedules are built
+    from: HBM counters recorded under one hash do not describe another."""
+    h = hashlib.sha256()
+    for path in sorted(glob.glob(os.path.join(ROOT, "paper_2609_33133_amd", "csrc", "*"))):
+        if path.endswith((".hip", ".h", ".cpp")):
+            h.update(os.path.basename(path).encode())
+            with open(path, "rb") as f:
+                h.update(f.read())
+    return h.hexdigest()[:16]
+
+
+_KNAME = re.compile(r"(attn_fwd_kernel|attn_dkv_kernel|attn_dq_kernel|bwd_dsum_kernel|lse_merge_kernel|"
+                    r"grad_reduce_kernel)(<([^>]*)>)?")
+
+
+def bench_kernel_name(rocprof_name: str):
+    """rocprofv3 kernel name -> the name used in the bench line (None for
+    kernels that are not the library's, e.g. runtime copies)."""
+    m = _KNAME.search(rocprof_name)
+    if not m:
+        return None
+    base, targs = m.group(1), (m.group(3) or "")
+    if base in ("attn_fwd_kernel", "attn_dkv_kernel"):
+        return base + ("<fp32 out>" if "true" in targs else "<bf16 out>")
+    return base
+
+
+def _counter_rows(path: str, counter: str):
+    out = []
+    with open(path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] == counter:
+                out.append((r["Kernel_Name"], float(r["Counter_Value"])))
+    return out
+
+
+def summarize_pmc(d: str, workload: str) -> str:
+    """Markdown summary (with a machine-readable line) of the FETCH_SIZE and
+    WRITE_SIZE passes in d/{fetch,write} and of the 1 GiB copy calibration
+    passes in d/{cfetch,cwrite} (rocprofv3 -f csv, file run_counter_collection.csv)."""
+    def rows(sub, counter):
+        return _counter_rows(os.path.join(d, sub, "run_counter_collection.csv"), counter)
+    copy_bytes = 1 << 30
+    cf = max(v for _, v in rows("cfetch", "FETCH_SIZE"))
+    cw = max(v for _, v in rows("cwrite", "WRITE_SIZE"))
+    f_scale = copy_bytes / (cf * 1024.0)
+    w_scale = copy_bytes / (cw * 1024.0)
+    per = {}
+    for sub, counter, scale, key in (("fetch", "FETCH_SIZE", f_scale, "fetch"), ("write", "WRITE_SIZE", w_scale, "write")):
+        for name, v in rows(sub, counter):
+            k = bench_kernel_name(name)
+            if k is None:
+                continue
+            e = per.setdefault(k, {"fetch": [], "write": []})
+            e[key].append(v * 1024.0 * scale)
+    kernels = {}
+    for k, e in per.items():
+        n = len(e["fetch"])
+        fb = sum(e["fetch"]) / max(n, 1)
+        wb = sum(e["write"]) / max(len(e["write"]), 1)
+        kernels[k] = {"launches": n, "fetch_bytes_per_launch": round(fb), "write_bytes_per_launch": round(wb),
+                      "bytes_per_launch": round(fb + wb)}
+    data = {"workload": workload, "source_hash": kernel_source_hash(),
+            "calibration": {"copy_bytes": copy_bytes, "copy_fetch_kib": cf, "copy_write_kib": cw,
+                            "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
+            "kernels": kernels}
+    lines = ["| kernel | launches | HBM read GB / launch | HBM write GB / launch |", "|---|---|---|---|"]
+    for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
+        lines.append(f"| {k} | {v['launches']} | {v['fetch_bytes_per_launch'] / 1e9:.3f} | "
+                     f"{v['write_bytes_per_launch'] / 1e9:.3f} |")
+    lines.append("")
+    lines.append(f"Copy calibration: a 1 GiB device copy reads {cf:.1f} KiB of FETCH_SIZE and writes {cw:.1f} KiB of "
+                 f"WRITE_SIZE per dispatch, so the factors are {f_scale:.4f} (read) and {w_scale:.4f} (write).")
+    lines.append("")
+    lines.append("<!-- traffic-json " + json.dumps(data, sort_keys=True) + " -->")
+    return "\n".join(lines)
+
+
+def summarize_trace(stats_csv: str) -> str:
+    """Markdown table of a rocprofv3 --kernel-trace --stats kernel_stats.csv."""
+    lines = ["| kernel | calls | total ms | avg ms | % |", "|---|---|---|---|---|"]
+    with open(stats_csv) as f:
+        for r in csv.DictReader(f):
+            name = r["Name"].replace("void ", "").replace("augtree::(anonymous namespace)::", "").split("(")[0]
+            lines.append(f"| {name} | {r['Calls']} | {int(r['TotalDurationNs']) / 1e6:.2f} | "
+                         f"{float(r['AverageNs']) / 1e6:.4f} | {float(r['Percentage']):.2f} |")
+    return "\n".join(lines)
+
+
+def recorded_traffic(workload: str, kernel: str):
+    """HBM bytes per launch of `kernel` from the committed counter summary of
+    this workload, or None when there is none or the kernel sources changed
+    since the counters were taken."""
+    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{WORKLOAD_SLUG[workload]}.md")
+    if not os.path.exists(path):
+        return None
+    with open(path) as f:
+        m = re.search(r"<!-- traffic-json (\{.*\}) -->", f.read())
+    if not m:
+        return None
+    data = json.loads(m.group(1))
+    if data.get("source_hash") != kernel_source_hash() or data.get("workload") != workload:
+        return None
+    k = data["kernels"].get(kernel)
+    return None if k is None else k["bytes_per_launch"]
 
 
 class KernelTimer:
@@ -179,10 +296,20 @@ def main():
     ap.add_argument("--n-seed", type=int, default=None)
     ap.add_argument("--no-flattened", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
-    ap.add_argument("--traffic", default=None, help="JSON file with measured HBM bytes per launch")
+    ap.add_argument("--summarize-pmc", default=None, metavar="DIR",
+                    help="print the HBM traffic summary of rocprofv3 counter passes in DIR/{fetch,write,cfetch,cwrite} "
+                         "(no GPU needed) and exit")
+    ap.add_argument("--summarize-trace", default=None, metavar="CSV",
+                    help="print a table of a rocprofv3 kernel_stats.csv (no GPU needed) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only run a 1 GiB device-to-device copy 3 times (HBM counter calibration) and exit")
     args = ap.parse_args()
+    if args.summarize_pmc:
+        print(summarize_pmc(args.summarize_pmc, args.workload))
+        return
+    if args.summarize_trace:
+        print(summarize_trace(args.summarize_trace))
+        return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
         print("bench.py measures one GPU: this build has no multi-GPU path (the hot path shards by whole "
               "groups or KV heads with no exchange inside the op); run with --gpus 1", file=sys.stderr)
@@ -250,10 +377,10 @@ def main():
     roof["kernel"] = dom_name
     roof["avg_launch_ms"] = round(avg_ms, 4)
     roof["launches_per_step"] = dom["launches"] // args.steps
-    roof["traffic"] = None
-    if args.traffic and os.path.exists(args.traffic):
-        with open(args.traffic) as f:
-            roof["traffic"] = json.load(f).get(dom_name)
+    # HBM bytes per launch measured by the FETCH_SIZE / WRITE_SIZE counter
+    # passes (copy-calibrated) on these exact sources, else null
+    roof["traffic"] = recorded_traffic(args.workload, dom_name)
+    roof["traffic_unit"] = "bytes per launch"
     kernel_table = {k: {"ms_per_step": round(v["ms"] / args.steps, 4),
                         ("TFLOP/s" if v["kind"] == "flop" else "GB/s"):
                             round(v["work"] / (v["ms"] * 1e-3) / (1e12 if v["kind"] == "flop" else 1e9), 2)}

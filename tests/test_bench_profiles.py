@@ -1,0 +1,77 @@
+"""bench.py's rocprofv3 summaries and the hash gate on recorded HBM traffic
+(CPU only: synthetic counter files)."""
+import csv
+import json
+import os
+import re
+import sys
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+sys.path.insert(0, ROOT)
+
+import bench  # noqa: E402
+
+FIELDS = ["Dispatch_Id", "Kernel_Name", "Counter_Name", "Counter_Value"]
+
+
+def _write(path, rows):
+    os.makedirs(os.path.dirname(path), exist_ok=True)
+    with open(path, "w", newline="") as f:
+        w = csv.DictWriter(f, fieldnames=FIELDS)
+        w.writeheader()
+        for r in rows:
+            w.writerow(dict(zip(FIELDS, r)))
+
+
+def test_kernel_names():
+    n = bench.bench_kernel_name
+    assert n("void augtree::(anonymous namespace)::attn_dkv_kernel<128, true>(augtree::DkvParams)") == \
+        "attn_dkv_kernel<fp32 out>"
+    assert n("void augtree::(anonymous namespace)::attn_fwd_kernel<64, false>(augtree::FwdParams)") == \
+        "attn_fwd_kernel<bf16 out>"
+    assert n("void augtree::(anonymous namespace)::attn_dq_kernel<128>(augtree::DqParams)") == "attn_dq_kernel"
+    assert n("__amd_rocclr_copyBuffer") is None
+
+
+def test_pmc_summary_scales_by_copy_calibration(tmp_path):
+    d = str(tmp_path)
+    k = "void augtree::(anonymous namespace)::attn_dkv_kernel<128, true>(augtree::DkvParams)"
+    # copy of 1 GiB reads 2^19 KiB of FETCH_SIZE (factor 2) and 2^20 KiB of WRITE_SIZE (factor 1)
+    _write(f"{d}/cfetch/run_counter_collection.csv", [(1, "copy", "FETCH_SIZE", 1 << 19)])
+    _write(f"{d}/cwrite/run_counter_collection.csv", [(1, "copy", "WRITE_SIZE", 1 << 20)])
+    _write(f"{d}/fetch/run_counter_collection.csv", [(1, k, "FETCH_SIZE", 1000.0), (2, k, "FETCH_SIZE", 3000.0),
+                                                     (3, "copy", "FETCH_SIZE", 5.0)])
+    _write(f"{d}/write/run_counter_collection.csv", [(1, k, "WRITE_SIZE", 10.0), (2, k, "WRITE_SIZE", 30.0)])
+    md = bench.summarize_pmc(d, "prompt")
+    data = json.loads(re.search(r"<!-- traffic-json (\{.*\}) -->", md).group(1))
+    e = data["kernels"]["attn_dkv_kernel<fp32 out>"]
+    assert e["launches"] == 2
+    assert e["fetch_bytes_per_launch"] == round(2000.0 * 1024 * 2)
+    assert e["write_bytes_per_launch"] == round(20.0 * 1024)
+    assert data["source_hash"] == bench.kernel_source_hash()
+
+
+def test_recorded_traffic_requires_matching_sources(tmp_path, monkeypatch):
+    prof = tmp_path / "profiles"
+    prof.mkdir()
+    data = {"workload": "prompt", "source_hash": bench.kernel_source_hash(),
+            "kernels": {"attn_dq_kernel": {"bytes_per_launch": 1234}}}
+    (prof / "hbm_traffic_prompt_P32768_G8.md").write_text("x\n<!-- traffic-json " + json.dumps(data) + " -->\n")
+    monkeypatch.setattr(bench, "ROOT", str(tmp_path))
+    # kernel_source_hash now sees no sources under tmp_path: a different hash
+    assert bench.recorded_traffic("prompt", "attn_dq_kernel") is None
+    monkeypatch.setattr(bench, "kernel_source_hash", lambda: data["source_hash"])
+    assert bench.recorded_traffic("prompt", "attn_dq_kernel") == 1234
+    assert bench.recorded_traffic("prompt", "attn_fwd_kernel<bf16 out>") is None
+    assert bench.recorded_traffic("balanced", "attn_dq_kernel") is None
+
+
+def test_trace_summary(tmp_path):
+    p = tmp_path / "stats.csv"
+    with open(p, "w", newline="") as f:
+        w = csv.writer(f)
+        w.writerow(["Name", "Calls", "TotalDurationNs", "AverageNs", "Percentage", "MinNs", "MaxNs", "StdDev"])
+        w.writerow(["void augtree::(anonymous namespace)::attn_dq_kernel<128>(augtree::DqParams)", 4, 4000000,
+                    1000000.0, 100.0, 1, 2, 0])
+    md = bench.summarize_trace(str(p))
+    assert "| attn_dq_kernel<128> | 4 | 4.00 | 1.0000 | 100.00 |" in md
