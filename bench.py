@@ -94,14 +94,18 @@ WORKLOAD_SLUG = {"tiny": "tiny_P256_G2", "balanced": "balanced_4groups_P4096_G8"
 
 
 def kernel_source_hash() -> str:
-    """Hash of every native source the kernels and their schedules are built
-    from: HBM counters recorded under one hash do not describe another."""
+    """Hash of the code (comments and whitespace removed) of every native
+    source the kernels and their schedules are built from: HBM counters
+    recorded under one hash do not describe another."""
     h = hashlib.sha256()
     for path in sorted(glob.glob(os.path.join(ROOT, "paper_2609_33133_amd", "csrc", "*"))):
         if path.endswith((".hip", ".h", ".cpp")):
+            with open(path) as f:
+                code = f.read()
+            code = re.sub(r"/\*.*?\*/", " ", code, flags=re.S)
+            code = re.sub(r"//[^\n]*", " ", code)
             h.update(os.path.basename(path).encode())
-            with open(path, "rb") as f:
-                h.update(f.read())
+            h.update(" ".join(code.split()).encode())
     return h.hexdigest()[:16]
 
 

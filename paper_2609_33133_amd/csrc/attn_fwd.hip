@@ -13,11 +13,13 @@
 // Q^T held in registers), the online-softmax update in fp32 with exp2 (the
 // output is rescaled only when a row maximum grows), and 16 MFMAs for
 // O^T += V^T P^T (V^T by transpose reads of the row-major V tile, P^T straight
-// from the S^T accumulators rounded to bf16). K and V tiles are
-// double-buffered in LDS (separate arrays, loop unrolled by two, so the
-// compiler can tell the buffer being filled from the one being read) and
-// copied there directly from global memory one block ahead
-// (global_load_lds), so no registers hold staged data.
+// from the S^T accumulators rounded to bf16). LDS addresses come from
+// per-lane offset tables computed once, and the operand reads run a few
+// MFMAs ahead of their MFMA. K and V tiles are double-buffered in LDS
+// (separate arrays, loop unrolled by two, so the compiler can tell the buffer
+// being filled from the one being read) and copied there directly from
+// global memory one block ahead (buffer_load ... lds), so no registers hold
+// staged data. Two workgroups share a CU (two wavefronts per SIMD).
 // The query heads of one KV head run on one XCD (shared K/V in its L2).
 #include "common.h"
 #include "kernels.h"
