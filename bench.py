@@ -47,6 +47,9 @@ WORKLOAD_TEXT = {
     "response": "response-dominant: 1 group, P=2048, G=16, R=16384, Hq=32, Hkv=8, d=128, seed 0",
     "ragged": "ragged: 16 groups, P log-uniform [512,65536], G in {4,8,16}, R log-uniform [256,32768], "
               "<=1,048,576 tokens, Hq=32, Hkv=8, d=128, seed 7",
+    **{f"gsweep{g}": f"group-size sweep: 1 group, P=8192, G={g}, R={65536 // g} (65,536 response tokens), "
+                     f"Hq=32, Hkv=8, d=128, seed 0" for g in (8, 16, 32, 64)},
+    "prompt_gqa7": "prompt-dominant, 7B-model heads: 1 group, P=32768, G=8, R=2048, Hq=28, Hkv=4 (g=7), d=128, seed 0",
 }
 
 # launch role -> compiled kernel (template instantiation) it runs
@@ -90,7 +93,9 @@ def role_work(role: str, shape, n_seed: int):
 
 # profiles/ file names per workload
 WORKLOAD_SLUG = {"tiny": "tiny_P256_G2", "balanced": "balanced_4groups_P4096_G8", "prompt": "prompt_P32768_G8",
-                 "response": "response_P2048_G16", "ragged": "ragged_16groups"}
+                 "response": "response_P2048_G16", "ragged": "ragged_16groups",
+                 **{f"gsweep{g}": f"gsweep_P8192_G{g}" for g in (8, 16, 32, 64)},
+                 "prompt_gqa7": "prompt_P32768_G8_H28_4"}
 
 
 def kernel_source_hash() -> str:

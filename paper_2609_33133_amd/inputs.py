@@ -121,7 +121,12 @@ def ragged_lengths(rng: np.random.Generator, num_groups: int = 16, cap: int = TO
 
 
 CONFIG_NAMES = ("tiny", "balanced", "prompt", "response", "ragged")
-CONFIG_SEEDS = {"tiny": 0, "balanced": 0, "prompt": 0, "response": 0, "ragged": 7}
+# Group-size sweep at a fixed 65,536 response tokens per tree (P = 8192,
+# G in {8, 16, 32, 64}, R = 65536 / G) and the prompt-heavy tree with the
+# 28 query / 4 KV heads of a 7B model (g = 7, not a power of two).
+SWEEP_NAMES = ("gsweep8", "gsweep16", "gsweep32", "gsweep64", "prompt_gqa7")
+CONFIG_SEEDS = {"tiny": 0, "balanced": 0, "prompt": 0, "response": 0, "ragged": 7,
+                **{n: 0 for n in SWEEP_NAMES}}
 
 
 def config_shape(name: str) -> GroupShape:
@@ -138,6 +143,11 @@ def config_shape(name: str) -> GroupShape:
         rng = np.random.Generator(np.random.PCG64(CONFIG_SEEDS["ragged"]))
         ps, rs, _ = ragged_lengths(rng)
         return GroupShape(ps, rs, 32, 8, 128)
+    if name.startswith("gsweep"):
+        g = int(name[len("gsweep"):])
+        return _fixed(8192, g, 65536 // g, 1, 32, 8, 128)
+    if name == "prompt_gqa7":
+        return _fixed(32768, 8, 2048, 1, 28, 4, 128)
     raise KeyError(name)
 
 

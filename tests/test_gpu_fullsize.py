@@ -50,7 +50,7 @@ def _host(t):
 
 
 @pytest.mark.timeout(900)
-@pytest.mark.parametrize("name", ["balanced", "prompt", "response", "ragged"])
+@pytest.mark.parametrize("name", ["balanced", "prompt", "response", "ragged", "gsweep64", "prompt_gqa7"])
 def test_fullsize_sampled(name):
     log(f"[fullsize] {name}: generating inputs")
     gi = I.make_config(name)

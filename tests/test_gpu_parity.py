@@ -41,6 +41,9 @@ SHAPES = [
     ([1, 2], [[1, 300], [5]], 4, 1, 128, 1.0),        # P = 1, R = 1, MQA
     ([64, 128, 192], [[64], [128], [192, 1]], 8, 2, 64, 1.0),
     ([500], [[40, 41, 42, 43]], 4, 2, 128, 4.0),      # very sharp
+    ([200, 33], [[100, 37, 64], [5]], 28, 4, 128, None),   # 28 / 4 heads: g = 7
+    ([130], [[70, 1, 129]], 28, 4, 128, 1.0),              # g = 7, sharp
+    ([96], [[3 + (7 * i) % 20 for i in range(64)]], 8, 2, 64, None),  # G = 64 short branches
 ]
 
 
