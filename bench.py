@@ -50,6 +50,7 @@ WORKLOAD_TEXT = {
     **{f"gsweep{g}": f"group-size sweep: 1 group, P=8192, G={g}, R={65536 // g} (65,536 response tokens), "
                      f"Hq=32, Hkv=8, d=128, seed 0" for g in (8, 16, 32, 64)},
     "prompt_gqa7": "prompt-dominant, 7B-model heads: 1 group, P=32768, G=8, R=2048, Hq=28, Hkv=4 (g=7), d=128, seed 0",
+    "short_resp": "short answers: 1 group, P=16384, G=32, R=64, Hq=32, Hkv=8, d=128, seed 0",
 }
 
 # launch role -> compiled kernel (template instantiation) it runs
@@ -59,20 +60,38 @@ ROLE_KERNEL = {
     "dkv_seed": "attn_dkv_kernel<fp32 out>", "dkv_prefill": "attn_dkv_kernel<fp32 out>",
     "dkv_resp": "attn_dkv_kernel<bf16 out>",
     "dq_replay": "attn_dq_kernel", "dq_prefill": "attn_dq_kernel",
-    "dsum": "bwd_dsum_kernel", "lse_merge": "lse_merge_kernel", "grad_reduce": "grad_reduce_kernel",
+    "dsum_replay": "bwd_dsum_kernel", "dsum_prefill": "bwd_dsum_kernel", "lse_merge": "lse_merge_kernel",
+    "grad_reduce": "grad_reduce_kernel",
+}
+# launch role -> step of the method (the prefill / replay time breakdown)
+ROLE_STEP = {
+    "fwd_prefill": "prefill_fwd", "fwd_replay": "replay_fwd", "fwd_replay_prompt": "replay_fwd",
+    "fwd_replay_own": "replay_fwd", "lse_merge": "replay_fwd", "dsum_replay": "replay_bwd", "dkv_seed": "replay_bwd",
+    "dkv_resp": "replay_bwd", "dq_replay": "replay_bwd", "dsum_prefill": "prefill_bwd", "dkv_prefill": "prefill_bwd",
+    "dq_prefill": "prefill_bwd", "grad_reduce": "prompt_grad_reduce",
 }
 # flops per (valid pair, query head) each attention role performs
 ROLE_FLOPS_PER_PAIR_D = {"fwd": 4, "dkv": 8, "dq": 6}
 
 
-def role_work(role: str, shape, n_seed: int):
-    """Algorithmic work of one launch: ('flop', F) for contractions, ('byte', B)
-    for the HBM-bound kernels."""
+def role_work(role: str, shape, n_seed: int, split=None):
+    """Algorithmic work of one step's launches of a role: ('flop', F) for
+    contractions, ('byte', B) for the HBM-bound kernels. `split` flags the
+    groups whose replay forward runs SPLIT (None: none of them)."""
     vp = shape.valid_pairs()
     hq, d = shape.num_q_heads, shape.head_dim
+    rp_split = rr_split = rows_split = 0
+    if split is not None:
+        for g, on in enumerate(split):
+            if on:
+                P, rs = shape.prompt_lens[g], shape.branch_lens[g]
+                rp_split += sum(r * P for r in rs)
+                rr_split += sum(r * (r + 1) // 2 for r in rs)
+                rows_split += sum(rs)
     pairs = {
-        "fwd_prefill": vp["prefill"], "fwd_replay": vp["replay_prompt"] + vp["replay_resp"],
-        "fwd_replay_prompt": vp["replay_prompt"], "fwd_replay_own": vp["replay_resp"],
+        "fwd_prefill": vp["prefill"],
+        "fwd_replay": vp["replay_prompt"] + vp["replay_resp"] - rp_split - rr_split,
+        "fwd_replay_prompt": rp_split, "fwd_replay_own": rr_split,
         "dkv_seed": vp["replay_prompt"], "dkv_resp": vp["replay_resp"], "dkv_prefill": vp["prefill"],
         "dq_replay": vp["replay_prompt"] + vp["replay_resp"], "dq_prefill": vp["prefill"],
     }
@@ -80,14 +99,14 @@ def role_work(role: str, shape, n_seed: int):
         per = ROLE_FLOPS_PER_PAIR_D[role.split("_")[0]]
         return "flop", float(per * d * hq * pairs[role])
     tp, tr, hkv = shape.total_prompt, shape.total_resp, shape.num_kv_heads
-    if role == "dsum":      # per launch (prompt and response launches averaged)
-        rows = (tp + tr) / 2.0
+    if role in ("dsum_replay", "dsum_prefill"):
+        rows = tr if role == "dsum_replay" else tp
         return "byte", float(rows * hq * (2 * d * 2 + 4))
     if role == "grad_reduce":
         e = 2 * tp * hkv * d
         return "byte", float(e * 4 * (1 + n_seed) + e * 2)
     if role == "lse_merge":
-        return "byte", float(tr * hq * (2 * d * 4 + 2 * 4 + d * 2 + 4))
+        return "byte", float(rows_split * hq * (2 * d * 4 + 2 * 4 + d * 2 + 4))
     raise KeyError(role)
 
 
@@ -95,7 +114,7 @@ def role_work(role: str, shape, n_seed: int):
 WORKLOAD_SLUG = {"tiny": "tiny_P256_G2", "balanced": "balanced_4groups_P4096_G8", "prompt": "prompt_P32768_G8",
                  "response": "response_P2048_G16", "ragged": "ragged_16groups",
                  **{f"gsweep{g}": f"gsweep_P8192_G{g}" for g in (8, 16, 32, 64)},
-                 "prompt_gqa7": "prompt_P32768_G8_H28_4"}
+                 "prompt_gqa7": "prompt_P32768_G8_H28_4", "short_resp": "short_P16384_G32_R64"}
 
 
 def kernel_source_hash() -> str:
@@ -301,7 +320,8 @@ def main():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=3)
     ap.add_argument("--workload", default="prompt", choices=sorted(WORKLOAD_TEXT))
-    ap.add_argument("--mode", default="fused", choices=("fused", "split"))
+    ap.add_argument("--mode", default="fused", choices=("fused", "split", "auto"),
+                    help="replay forward: fused, split, or per group by the library's cost rule")
     ap.add_argument("--n-seed", type=int, default=None)
     ap.add_argument("--no-flattened", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
@@ -328,7 +348,8 @@ def main():
 
     from paper_2609_33133_amd import _lib
     from paper_2609_33133_amd import inputs as I
-    from paper_2609_33133_amd.api import REPLAY_FUSED, REPLAY_SPLIT, GroupBatch
+    from paper_2609_33133_amd import api
+    from paper_2609_33133_amd.api import REPLAY_AUTO, REPLAY_FUSED, REPLAY_SPLIT, GroupBatch
     from paper_2609_33133_amd.group_attention import FlattenedStep, SharedStep, upload
 
     lib = _lib.load()
@@ -349,7 +370,7 @@ def main():
     s = gi.shape
     b = GroupBatch.from_shape(s)
     x = upload(gi, "cuda:0")
-    mode = REPLAY_FUSED if args.mode == "fused" else REPLAY_SPLIT
+    mode = {"fused": REPLAY_FUSED, "split": REPLAY_SPLIT, "auto": REPLAY_AUTO}[args.mode]
     step = SharedStep(b, "cuda:0", mode=mode, n_seed=args.n_seed)
     vp = s.valid_pairs()
     counted = 14.0 * s.head_dim * s.num_q_heads * vp["shared"]
@@ -364,14 +385,21 @@ def main():
             step.run(x)
         torch.cuda.synchronize()
     per_role = kt.summary()
-    kernels = {}
+    split = None
+    if mode == REPLAY_SPLIT:
+        split = [1] * s.num_groups
+    elif mode == REPLAY_AUTO:
+        split = [int(v) for v in api.replay_split_groups(b)]
+    kernels, breakdown = {}, {}
     for role, times in per_role.items():
         k = ROLE_KERNEL[role]
-        kind, work = role_work(role, s, step.n_seed)
+        kind, work = role_work(role, s, step.n_seed, split)
         e = kernels.setdefault(k, {"ms": 0.0, "launches": 0, "work": 0.0, "kind": kind})
         e["ms"] += float(np.sum(times))
         e["launches"] += len(times)
-        e["work"] += work * len(times)
+        e["work"] += work * args.steps
+        st = ROLE_STEP[role]
+        breakdown[st] = breakdown.get(st, 0.0) + float(np.sum(times)) / args.steps
     dom_name, dom = max(kernels.items(), key=lambda kv: kv[1]["ms"])
     avg_ms = dom["ms"] / dom["launches"]
     per_launch = dom["work"] / dom["launches"]
@@ -425,6 +453,9 @@ def main():
         "host_wall_ms_per_step": round(wall_ms, 4),
         "roofline": roof,
         "kernels": kernel_table,
+        # time per step of each step of the method (prefill vs replay), from the per-launch events
+        "breakdown_ms": {k: round(v, 4) for k, v in breakdown.items()},
+        "replay_split_groups": None if split is None else int(sum(split)),
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

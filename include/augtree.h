@@ -72,7 +72,8 @@ typedef enum augtree_status {
 
 typedef enum augtree_replay_mode {
   AUGTREE_REPLAY_FUSED = 0, /* prompt sweep then own-branch sweep, merged in registers */
-  AUGTREE_REPLAY_SPLIT = 1  /* two partial states written out, then lse_merge */
+  AUGTREE_REPLAY_SPLIT = 1, /* two partial states written out, then lse_merge */
+  AUGTREE_REPLAY_AUTO = 2   /* per group, FUSED or SPLIT by a cost rule (augtree_replay_split_groups) */
 } augtree_replay_mode;
 
 typedef enum augtree_op {
@@ -132,8 +133,12 @@ int augtree_prefill_fwd(const augtree_groups* grp, const uint16_t* q_p, const ui
  * FUSED: one sweep over both key sets, merged in registers.
  * SPLIT: partial A and partial B are written to o_part [2][T_R,Hq,d] fp32 and
  *   lse_part [2][Hq,T_R] fp32 (part 0 = prompt, part 1 = own branch), then
- *   merged by the lse_merge kernel into o_r / lse_r. In FUSED mode o_part and
- *   lse_part may be NULL.
+ *   merged by the lse_merge kernel into o_r / lse_r. The prompt partial's
+ *   query tiles pack the rows of all branches of a group (they all see the
+ *   same prompt keys), so short branches do not leave tiles mostly empty.
+ * AUTO: each group runs FUSED or SPLIT as augtree_replay_split_groups reports;
+ *   o_part / lse_part are required (only the split groups' rows are written
+ *   there). In FUSED mode o_part and lse_part may be NULL.
  * In:  q_r [T_R,Hq,d], k_r, v_r [T_R,Hkv,d], k_p, v_p [T_P,Hkv,d] bf16.
  * Out: o_r [T_R,Hq,d] bf16, lse_r [Hq,T_R] fp32.
  */
@@ -141,6 +146,21 @@ int augtree_replay_fwd(const augtree_groups* grp, int mode, const uint16_t* q_r,
                        const uint16_t* v_r, const uint16_t* k_p, const uint16_t* v_p, uint16_t* o_r,
                        float* lse_r, float* o_part, float* lse_part, void* ws, size_t ws_bytes,
                        void* stream);
+
+/*
+ * The replay-forward mode AUGTREE_REPLAY_AUTO gives each group (the choice of
+ * a way to run one step of §3.2 per group, like the per-tree primitive choice
+ * of §3.4, made here from the kernels' own costs). Writes split[g] = 1 when
+ * group g runs SPLIT, 0 when FUSED. The rule: a mode costs the number of
+ * (query tile, 64-key block) steps its forward tiles execute at a measured
+ * time per step, plus, for SPLIT, the merge's HBM bytes at a measured
+ * bandwidth; SPLIT is taken when it costs less. Short branches favour SPLIT
+ * (a fused tile of a 16-row branch sweeps every prompt block for 16 rows),
+ * long ones FUSED (same steps, no merge).
+ * In:  grp (host offsets). Out: split [num_groups] int32, host memory.
+ * Errors: INVALID_ARGUMENT for a bad descriptor or a NULL split.
+ */
+int augtree_replay_split_groups(const augtree_groups* grp, int32_t* split);
 
 /*
  * Merge of n partial softmax states of the same rows (§3.3, the associative
@@ -224,7 +244,7 @@ int augtree_prompt_grad_reduce(int32_t n_tensors, int64_t rows, int32_t heads, i
  * called on the calling thread immediately before (phase 0) and after
  * (phase 1) every kernel launch the library enqueues from that thread, with a
  * static role name ("fwd_prefill", "fwd_replay", "fwd_replay_prompt",
- * "fwd_replay_own", "lse_merge", "dsum", "dkv_seed", "dkv_resp",
+ * "fwd_replay_own", "lse_merge", "dsum_replay", "dsum_prefill", "dkv_seed", "dkv_resp",
  * "dkv_prefill", "dq_replay", "dq_prefill", "grad_reduce") and the stream the
  * kernel is enqueued on, so that a caller can record HIP events around single
  * kernels. The hook must not call back into the library. NULL removes it.

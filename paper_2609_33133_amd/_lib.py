@@ -23,6 +23,7 @@ AUGTREE_ERR_HIP = 6
 
 REPLAY_FUSED = 0
 REPLAY_SPLIT = 1
+REPLAY_AUTO = 2
 
 OP_PREFILL_FWD = 0
 OP_REPLAY_FWD = 1
@@ -33,6 +34,7 @@ EXPORTS = (
     "augtree_workspace_size", "augtree_prefill_fwd", "augtree_replay_fwd", "augtree_lse_merge",
     "augtree_replay_bwd", "augtree_prefill_bwd", "augtree_prompt_grad_reduce", "augtree_status_string",
     "augtree_last_error", "augtree_check_device", "augtree_version", "augtree_set_launch_hook",
+    "augtree_replay_split_groups",
 )
 
 LAUNCH_HOOK = ctypes.CFUNCTYPE(None, ctypes.c_char_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p)
@@ -82,6 +84,7 @@ def _sig(lib):
         "augtree_check_device": (ctypes.c_int, []),
         "augtree_version": (ctypes.c_char_p, []),
         "augtree_set_launch_hook": (None, [LAUNCH_HOOK, ctypes.c_void_p]),
+        "augtree_replay_split_groups": (ctypes.c_int, [_GP, _P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)

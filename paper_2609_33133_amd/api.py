@@ -16,7 +16,7 @@ import numpy as np
 import torch
 
 from . import _lib
-from ._lib import REPLAY_FUSED, REPLAY_SPLIT, OP_PREFILL_FWD, OP_REPLAY_FWD, OP_PREFILL_BWD, OP_REPLAY_BWD  # noqa: F401
+from ._lib import REPLAY_FUSED, REPLAY_SPLIT, REPLAY_AUTO, OP_PREFILL_FWD, OP_REPLAY_FWD, OP_PREFILL_BWD, OP_REPLAY_BWD  # noqa: F401
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -110,7 +110,7 @@ def replay_fwd(b: GroupBatch, q_r, k_r, v_r, k_p, v_p, mode: int = REPLAY_FUSED,
     dev = q_r.device
     o_r = torch.empty_like(q_r) if o_r is None else o_r
     lse_r = torch.empty((b.hq, b.tr), dtype=torch.float32, device=dev) if lse_r is None else lse_r
-    if mode == REPLAY_SPLIT:
+    if mode != REPLAY_FUSED:
         o_part = torch.empty((2, b.tr, b.hq, b.d), dtype=torch.float32, device=dev) if o_part is None else o_part
         lse_part = torch.empty((2, b.hq, b.tr), dtype=torch.float32, device=dev) if lse_part is None else lse_part
     ws, nws = _ws(b, ws, OP_REPLAY_FWD, mode, dev)
@@ -118,6 +118,14 @@ def replay_fwd(b: GroupBatch, q_r, k_r, v_r, k_p, v_p, mode: int = REPLAY_FUSED,
                                               _ptr(o_r), _ptr(lse_r), _ptr(o_part), _ptr(lse_part), _ptr(ws), nws,
                                               _stream(stream)), "replay_fwd")
     return o_r, lse_r, o_part, lse_part
+
+
+def replay_split_groups(b: GroupBatch) -> np.ndarray:
+    """Per group, 1 if AUGTREE_REPLAY_AUTO runs it SPLIT, 0 if FUSED."""
+    out = np.zeros(b.num_groups, dtype=np.int32)
+    _lib.check(_lib.load().augtree_replay_split_groups(b.ref, out.ctypes.data_as(ctypes.c_void_p)),
+               "replay_split_groups")
+    return out
 
 
 def lse_merge(o_parts, lse_parts, o=None, o_f32=None, lse=None, want_bf16=True, stream=None):

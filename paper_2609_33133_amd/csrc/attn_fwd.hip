@@ -209,5 +209,6 @@ hipError_t launch_attn_fwd(const FwdParams& p0, int n_tiles, bool out_f32, hipSt
 }
 
 int fwd_block_m() { return BM; }
+int fwd_block_n() { return BN; }
 
 }  // namespace augtree

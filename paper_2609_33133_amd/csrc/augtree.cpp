@@ -185,9 +185,11 @@ std::vector<QTile> prefill_qtiles(const Shape& s, int bm) {
 // part 1 = own-branch causal keys only, fused = both
 enum { RP_PROMPT = 0, RP_OWN = 1, RP_FUSED = 2 };
 
-std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which) {
+// `keep` (optional, one flag per group) limits the tiles to the flagged groups
+std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which, const std::vector<char>* keep = nullptr) {
   std::vector<QTile> v;
   for (int g = 0; g < s.ng; ++g) {
+    if (keep && !(*keep)[g]) continue;
     const int P = s.cp[g + 1] - s.cp[g];
     if (which == RP_PROMPT) {
       const int r0 = s.cr[s.cb[g]], r1 = s.cr[s.cb[g + 1]];
@@ -219,6 +221,42 @@ std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which) {
     }
   }
   sort_by_cost(v, qtile_cost);
+  return v;
+}
+
+// Replay forward mode per group (AUGTREE_REPLAY_AUTO). A mode's cost is the
+// number of (query tile, 64-key block) steps its forward tiles execute, at the
+// measured time of one step per workgroup slot of the chip, plus for SPLIT
+// the HBM time of the merge. A fused tile of a short branch sweeps every
+// prompt block for a few rows; the split prompt partial packs the rows of all
+// branches of the group into full tiles, but pays the partials' round trip.
+constexpr double kFwdStepNs = 3.7;         // 128 rows x 64 keys x one head, d = 128, per slot (measured)
+constexpr double kMergeBytesPerNs = 5000;  // merge kernel bandwidth (measured, ~5 TB/s)
+
+int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool replay_prefers_split(const Shape& s, int g, int bm, int bn) {
+  const int64_t prompt_blocks = ceil_div(s.cp[g + 1] - s.cp[g], bn);
+  int64_t fused = 0, own = 0, rows = 0;
+  for (int b = s.cb[g]; b < s.cb[g + 1]; ++b) {
+    const int R = s.cr[b + 1] - s.cr[b];
+    rows += R;
+    for (int t0 = 0; t0 < R; t0 += bm) {
+      const int64_t own_blocks = ceil_div(std::min(R, t0 + bm), bn);
+      fused += prompt_blocks + own_blocks;
+      own += own_blocks;
+    }
+  }
+  const int64_t split = ceil_div(rows, bm) * prompt_blocks + own;
+  const double step = kFwdStepNs * (double)s.d / 128.0 * s.hq;
+  const double merge_bytes = (double)rows * s.hq * (10.0 * s.d + 12.0);
+  return split * step + merge_bytes / kMergeBytesPerNs < fused * step;
+}
+
+std::vector<char> replay_split_groups(const Shape& s, int mode) {
+  std::vector<char> v(s.ng, mode == AUGTREE_REPLAY_SPLIT ? 1 : 0);
+  if (mode == AUGTREE_REPLAY_AUTO)
+    for (int g = 0; g < s.ng; ++g) v[g] = replay_prefers_split(s, g, fwd_block_m(), fwd_block_n()) ? 1 : 0;
   return v;
 }
 
@@ -290,9 +328,9 @@ constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 struct Plan {
-  std::vector<QTile> q1, q2;      // forward / dQ tiles (q2: second list of split mode)
+  std::vector<QTile> q1, q2, q3;  // forward / dQ tiles (split: q1 prompt, q2 own; auto: q3 fused groups)
   std::vector<KVTile> kv1, kv2;   // dK/dV tiles
-  size_t off_q1 = 0, off_q2 = 0, off_kv1 = 0, off_kv2 = 0, off_dsum = 0, bytes = 0;
+  size_t off_q1 = 0, off_q2 = 0, off_q3 = 0, off_kv1 = 0, off_kv2 = 0, off_dsum = 0, bytes = 0;
   int64_t dsum_rows = 0;
   std::vector<char> blob;         // schedule bytes copied to the start of the workspace
   size_t blob_bytes = 0;
@@ -301,6 +339,7 @@ struct Plan {
     size_t o = 0;
     off_q1 = o; o = align_up(o + q1.size() * sizeof(QTile));
     off_q2 = o; o = align_up(o + q2.size() * sizeof(QTile));
+    off_q3 = o; o = align_up(o + q3.size() * sizeof(QTile));
     off_kv1 = o; o = align_up(o + kv1.size() * sizeof(KVTile));
     off_kv2 = o; o = align_up(o + kv2.size() * sizeof(KVTile));
     blob_bytes = o;
@@ -311,6 +350,7 @@ struct Plan {
     blob.assign(blob_bytes, 0);
     if (!q1.empty()) std::memcpy(blob.data() + off_q1, q1.data(), q1.size() * sizeof(QTile));
     if (!q2.empty()) std::memcpy(blob.data() + off_q2, q2.data(), q2.size() * sizeof(QTile));
+    if (!q3.empty()) std::memcpy(blob.data() + off_q3, q3.data(), q3.size() * sizeof(QTile));
     if (!kv1.empty()) std::memcpy(blob.data() + off_kv1, kv1.data(), kv1.size() * sizeof(KVTile));
     if (!kv2.empty()) std::memcpy(blob.data() + off_kv2, kv2.data(), kv2.size() * sizeof(KVTile));
   }
@@ -326,6 +366,13 @@ Plan plan_for(const Shape& s, int op, int arg) {
       if (arg == AUGTREE_REPLAY_SPLIT) {
         pl.q1 = replay_qtiles(s, fwd_block_m(), RP_PROMPT);
         pl.q2 = replay_qtiles(s, fwd_block_m(), RP_OWN);
+      } else if (arg == AUGTREE_REPLAY_AUTO) {
+        const std::vector<char> split = replay_split_groups(s, arg);
+        std::vector<char> fused(split.size());
+        for (size_t g = 0; g < split.size(); ++g) fused[g] = !split[g];
+        pl.q1 = replay_qtiles(s, fwd_block_m(), RP_PROMPT, &split);
+        pl.q2 = replay_qtiles(s, fwd_block_m(), RP_OWN, &split);
+        pl.q3 = replay_qtiles(s, fwd_block_m(), RP_FUSED, &fused);
       } else {
         pl.q1 = replay_qtiles(s, fwd_block_m(), RP_FUSED);
       }
@@ -417,7 +464,8 @@ size_t augtree_workspace_size(const augtree_groups* grp, int op, int arg) {
     fail(AUGTREE_ERR_INVALID_ARGUMENT, "unknown op %d", op);
     return 0;
   }
-  if (op == AUGTREE_OP_REPLAY_FWD && arg != AUGTREE_REPLAY_FUSED && arg != AUGTREE_REPLAY_SPLIT) {
+  if (op == AUGTREE_OP_REPLAY_FWD && arg != AUGTREE_REPLAY_FUSED && arg != AUGTREE_REPLAY_SPLIT &&
+      arg != AUGTREE_REPLAY_AUTO) {
     fail(AUGTREE_ERR_INVALID_ARGUMENT, "unknown replay mode %d", arg);
     return 0;
   }
@@ -459,11 +507,11 @@ int augtree_replay_fwd(const augtree_groups* grp, int mode, const uint16_t* q_r,
   Shape s;
   int st = validate_groups(grp, &s);
   if (st) return st;
-  if (mode != AUGTREE_REPLAY_FUSED && mode != AUGTREE_REPLAY_SPLIT)
+  if (mode != AUGTREE_REPLAY_FUSED && mode != AUGTREE_REPLAY_SPLIT && mode != AUGTREE_REPLAY_AUTO)
     return fail(AUGTREE_ERR_INVALID_ARGUMENT, "unknown replay mode %d", mode);
   REQUIRE_PTR(q_r); REQUIRE_PTR(k_r); REQUIRE_PTR(v_r); REQUIRE_PTR(k_p); REQUIRE_PTR(v_p);
   REQUIRE_PTR(o_r); REQUIRE_PTR(lse_r);
-  if (mode == AUGTREE_REPLAY_SPLIT) { REQUIRE_PTR(o_part); REQUIRE_PTR(lse_part); }
+  if (mode != AUGTREE_REPLAY_FUSED) { REQUIRE_PTR(o_part); REQUIRE_PTR(lse_part); }
   Plan pl = plan_for(s, AUGTREE_OP_REPLAY_FWD, mode);
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
   if ((st = check_device_impl())) return st;
@@ -474,35 +522,55 @@ int augtree_replay_fwd(const augtree_groups* grp, int mode, const uint16_t* q_r,
   p.lse_rows = s.tr;
   p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d;
   p.scale_log2 = log2e_scale(s.scale);
-  if (mode == AUGTREE_REPLAY_FUSED) {
-    p.tiles = at<QTile>(ws, pl.off_q1);
+  // fused tiles: all groups (FUSED) or the groups the cost rule keeps fused (AUTO)
+  const std::vector<QTile>& fused_tiles = mode == AUGTREE_REPLAY_FUSED ? pl.q1 : pl.q3;
+  const size_t fused_off = mode == AUGTREE_REPLAY_FUSED ? pl.off_q1 : pl.off_q3;
+  if (!fused_tiles.empty()) {
+    p.tiles = at<QTile>(ws, fused_off);
     p.o = o_r; p.lse = lse_r;
-    {
-      HookScope h("fwd_replay", str);
-      if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), false, str), "replay fwd launch"))) return st;
-    }
-    return ok();
+    HookScope h("fwd_replay", str);
+    if ((st = hip_status(launch_attn_fwd(p, (int)fused_tiles.size(), false, str), "replay fwd launch"))) return st;
   }
+  if (mode == AUGTREE_REPLAY_FUSED) return ok();
+  // split groups: two partial states, then the merge over their rows
   const int64_t part_o = s.tr * s.hq * s.d;
   const int64_t part_l = s.tr * s.hq;
-  p.tiles = at<QTile>(ws, pl.off_q1);
-  p.o32 = o_part; p.lse = lse_part;
-  {
+  p.o = nullptr;
+  if (!pl.q1.empty()) {
+    p.tiles = at<QTile>(ws, pl.off_q1);
+    p.o32 = o_part; p.lse = lse_part;
     HookScope h("fwd_replay_prompt", str);
     if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), true, str), "replay prompt partial launch"))) return st;
   }
-  p.tiles = at<QTile>(ws, pl.off_q2);
-  p.o32 = o_part + part_o; p.lse = lse_part + part_l;
-  {
+  if (!pl.q2.empty()) {
+    p.tiles = at<QTile>(ws, pl.off_q2);
+    p.o32 = o_part + part_o; p.lse = lse_part + part_l;
     HookScope h("fwd_replay_own", str);
     if ((st = hip_status(launch_attn_fwd(p, (int)pl.q2.size(), true, str), "replay own partial launch"))) return st;
   }
-  {
+  const std::vector<char> split = replay_split_groups(s, mode);
+  for (int g = 0; g < s.ng;) {  // one merge per run of consecutive split groups (contiguous rows)
+    if (!split[g]) { ++g; continue; }
+    int g1 = g;
+    while (g1 < s.ng && split[g1]) ++g1;
+    const int64_t r0 = s.cr[s.cb[g]], r1 = s.cr[s.cb[g1]];
     HookScope h("lse_merge", str);
-    if ((st = hip_status(launch_lse_merge(s.tr, s.hq, s.d, 2, o_part, lse_part, o_r, nullptr, lse_r, str),
+    if ((st = hip_status(launch_lse_merge(r0, r1 - r0, s.tr, s.hq, s.d, 2, o_part, lse_part, o_r, nullptr, lse_r,
+                                          str),
                          "lse merge launch")))
       return st;
+    g = g1;
   }
+  return ok();
+}
+
+int augtree_replay_split_groups(const augtree_groups* grp, int32_t* split) {
+  Shape s;
+  int st = validate_groups(grp, &s);
+  if (st) return st;
+  if (!split) return fail(AUGTREE_ERR_INVALID_ARGUMENT, "null pointer: split");
+  const std::vector<char> v = replay_split_groups(s, AUGTREE_REPLAY_AUTO);
+  for (int g = 0; g < s.ng; ++g) split[g] = v[g];
   return ok();
 }
 
@@ -518,7 +586,7 @@ int augtree_lse_merge(int64_t rows, int32_t heads, int32_t head_dim, int32_t n_p
   int st;
   if ((st = check_device_impl())) return st;
   HookScope h("lse_merge", static_cast<hipStream_t>(stream));
-  if ((st = hip_status(launch_lse_merge(rows, heads, head_dim, n_parts, o_parts, lse_parts, o, o_f32, lse,
+  if ((st = hip_status(launch_lse_merge(0, rows, rows, heads, head_dim, n_parts, o_parts, lse_parts, o, o_f32, lse,
                                         static_cast<hipStream_t>(stream)),
                        "lse merge launch")))
     return st;
@@ -543,7 +611,7 @@ int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uin
   if ((st = upload(pl, ws, str))) return st;
   float* dsum = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_dsum);
   {
-    HookScope h("dsum", str);
+    HookScope h("dsum_replay", str);
     if ((st = hip_status(launch_bwd_dsum(o_r, do_r, dsum, s.tr, s.hq, s.d, str), "dsum launch"))) return st;
   }
   const float sl2 = log2e_scale(s.scale);
@@ -595,7 +663,7 @@ int augtree_prefill_bwd(const augtree_groups* grp, const uint16_t* q_p, const ui
   if ((st = upload(pl, ws, str))) return st;
   float* dsum = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_dsum);
   {
-    HookScope h("dsum", str);
+    HookScope h("dsum_prefill", str);
     if ((st = hip_status(launch_bwd_dsum(o_p, do_p, dsum, s.tp, s.hq, s.d, str), "dsum launch"))) return st;
   }
   const float sl2 = log2e_scale(s.scale);

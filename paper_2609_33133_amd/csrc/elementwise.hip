@@ -9,25 +9,29 @@ namespace {
 
 typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
 
-// One thread per (row, head, 8-element chunk). The part LSEs of a (row, head)
-// are read by each of its chunk threads (same cache lines). Parts are visited
-// in index order, so the result does not depend on the launch.
-__global__ __launch_bounds__(256) void lse_merge_kernel(int64_t rows, int heads, int head_dim, int n_parts,
+// One thread per (row, head, 8-element chunk) of rows row0 .. row0 + rows - 1
+// of tensors with total_rows rows (o parts [n][total_rows, heads, d], lse
+// parts [n][heads][total_rows], outputs likewise). The part LSEs of a
+// (row, head) are read by each of its chunk threads (same cache lines). Parts
+// are visited in index order, so the result does not depend on the launch.
+__global__ __launch_bounds__(256) void lse_merge_kernel(int64_t row0, int64_t rows, int64_t total_rows, int heads,
+                                                        int head_dim, int n_parts,
                                                         const float* __restrict__ o_parts,
                                                         const float* __restrict__ lse_parts,
                                                         uint16_t* __restrict__ o, float* __restrict__ o32,
                                                         float* __restrict__ lse) {
   const int ch_per_row = head_dim / 8;
   const int64_t total = rows * heads * ch_per_row;
-  const int64_t part_o = rows * heads * head_dim;
-  const int64_t part_l = rows * heads;
+  const int64_t part_o = total_rows * heads * head_dim;
+  const int64_t part_l = total_rows * heads;
   for (int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; gid < total;
        gid += (int64_t)gridDim.x * blockDim.x) {
-    const int64_t rh = gid / ch_per_row;
-    const int ch = (int)(gid - rh * ch_per_row);
-    const int64_t row = rh / heads;
-    const int h = (int)(rh - row * heads);
-    const int64_t lidx = (int64_t)h * rows + row;
+    const int64_t rh_local = gid / ch_per_row;
+    const int ch = (int)(gid - rh_local * ch_per_row);
+    const int64_t row = row0 + rh_local / heads;
+    const int h = (int)(rh_local - (row - row0) * heads);
+    const int64_t rh = row * heads + h;
+    const int64_t lidx = (int64_t)h * total_rows + row;
     float m = -INFINITY;
     for (int k = 0; k < n_parts; ++k) m = fmaxf(m, lse_parts[k * part_l + lidx]);
     float acc[8];
@@ -102,12 +106,13 @@ unsigned grid_for(int64_t threads) {
 
 }  // namespace
 
-hipError_t launch_lse_merge(int64_t rows, int heads, int head_dim, int n_parts, const float* o_parts,
-                            const float* lse_parts, uint16_t* o, float* o32, float* lse, hipStream_t stream) {
+hipError_t launch_lse_merge(int64_t row0, int64_t rows, int64_t total_rows, int heads, int head_dim, int n_parts,
+                            const float* o_parts, const float* lse_parts, uint16_t* o, float* o32, float* lse,
+                            hipStream_t stream) {
   const int64_t threads = rows * heads * (head_dim / 8);
   if (threads == 0) return hipSuccess;
-  hipLaunchKernelGGL(lse_merge_kernel, dim3(grid_for(threads)), dim3(256), 0, stream, rows, heads, head_dim,
-                     n_parts, o_parts, lse_parts, o, o32, lse);
+  hipLaunchKernelGGL(lse_merge_kernel, dim3(grid_for(threads)), dim3(256), 0, stream, row0, rows, total_rows, heads,
+                     head_dim, n_parts, o_parts, lse_parts, o, o32, lse);
   return hipGetLastError();
 }
 

@@ -64,13 +64,16 @@ hipError_t launch_attn_dq(const DqParams& p, int n_tiles, hipStream_t stream);
 hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, bool out_f32, hipStream_t stream);
 hipError_t launch_bwd_dsum(const uint16_t* o, const uint16_t* dout, float* dsum, int64_t rows, int hq,
                            int head_dim, hipStream_t stream);
-hipError_t launch_lse_merge(int64_t rows, int heads, int head_dim, int n_parts, const float* o_parts,
-                            const float* lse_parts, uint16_t* o, float* o32, float* lse, hipStream_t stream);
+// rows row0 .. row0 + rows - 1 of [total_rows]-row tensors
+hipError_t launch_lse_merge(int64_t row0, int64_t rows, int64_t total_rows, int heads, int head_dim, int n_parts,
+                            const float* o_parts, const float* lse_parts, uint16_t* o, float* o32, float* lse,
+                            hipStream_t stream);
 hipError_t launch_grad_reduce(int n_tensors, int64_t rows, int64_t row_elems, const float* self, int n_parts,
                               int64_t part_rows, int64_t part_stride, const float* parts, const int32_t* row_map, uint16_t* out,
                               float* out32, hipStream_t stream);
 
 int fwd_block_m();
+int fwd_block_n();
 int dq_block_m();
 int dkv_block_n();
 int dkv_block_q();

@@ -22,7 +22,7 @@ import numpy as np
 import torch
 
 from . import api
-from .api import REPLAY_FUSED, REPLAY_SPLIT, GroupBatch
+from .api import REPLAY_AUTO, REPLAY_FUSED, REPLAY_SPLIT, GroupBatch
 
 TENSORS = ("q_p", "k_p", "v_p", "q_r", "k_r", "v_r", "do_p", "do_r")
 
@@ -60,7 +60,7 @@ class SharedStep:
         self.o_r = torch.empty((b.tr, b.hq, b.d), dtype=bf, device=dev)
         self.lse_r = torch.empty((b.hq, b.tr), dtype=f32, device=dev)
         self.o_part = self.lse_part = None
-        if mode == REPLAY_SPLIT:
+        if mode != REPLAY_FUSED:
             self.o_part = torch.empty((2, b.tr, b.hq, b.d), dtype=f32, device=dev)
             self.lse_part = torch.empty((2, b.hq, b.tr), dtype=f32, device=dev)
         self.dq_r = torch.empty((b.tr, b.hq, b.d), dtype=bf, device=dev)

@@ -123,8 +123,10 @@ def ragged_lengths(rng: np.random.Generator, num_groups: int = 16, cap: int = TO
 CONFIG_NAMES = ("tiny", "balanced", "prompt", "response", "ragged")
 # Group-size sweep at a fixed 65,536 response tokens per tree (P = 8192,
 # G in {8, 16, 32, 64}, R = 65536 / G) and the prompt-heavy tree with the
-# 28 query / 4 KV heads of a 7B model (g = 7, not a power of two).
-SWEEP_NAMES = ("gsweep8", "gsweep16", "gsweep32", "gsweep64", "prompt_gqa7")
+# 28 query / 4 KV heads of a 7B model (g = 7, not a power of two), and a
+# short-answer tree (P = 16384, G = 32, R = 64) where the replay forward's
+# per-group mode rule chooses the split form.
+SWEEP_NAMES = ("gsweep8", "gsweep16", "gsweep32", "gsweep64", "prompt_gqa7", "short_resp")
 CONFIG_SEEDS = {"tiny": 0, "balanced": 0, "prompt": 0, "response": 0, "ragged": 7,
                 **{n: 0 for n in SWEEP_NAMES}}
 
@@ -148,6 +150,8 @@ def config_shape(name: str) -> GroupShape:
         return _fixed(8192, g, 65536 // g, 1, 32, 8, 128)
     if name == "prompt_gqa7":
         return _fixed(32768, 8, 2048, 1, 28, 4, 128)
+    if name == "short_resp":
+        return _fixed(16384, 32, 64, 1, 32, 8, 128)
     raise KeyError(name)
 
 

@@ -219,3 +219,25 @@ def test_flattened_baseline_matches_oracle():
     ref = oracle(gi)
     got = run_flattened(gi)
     assert_close(got, ref, "flattened")
+
+
+def test_auto_mode_mixed_groups():
+    """AUGTREE_REPLAY_AUTO runs short-branch groups SPLIT and long-branch
+    groups FUSED in one call; every output against the oracle."""
+    shape = I.custom_shape([700, 130, 256], [[5] * 12, [200, 129], [17] * 4], 8, 2, 128)
+    b = GroupBatch.from_shape(shape)
+    assert api.replay_split_groups(b).tolist() == [1, 0, 1]
+    gi = I.make_inputs(shape, seed=41, qk_mult=1.0)
+    ref = oracle(gi)
+    got, _ = run_shared(gi, mode=api.REPLAY_AUTO)
+    assert_close(got, ref, "auto mixed")
+
+
+@pytest.mark.parametrize("ps,rs,same_as", [([300], [[250, 260]], REPLAY_FUSED), ([1000], [[3] * 20], REPLAY_SPLIT)])
+def test_auto_mode_equals_chosen_mode_bitwise(ps, rs, same_as):
+    shape = I.custom_shape(ps, rs, 8, 2, 128)
+    gi = I.make_inputs(shape, seed=42)
+    a, _ = run_shared(gi, mode=api.REPLAY_AUTO)
+    m, _ = run_shared(gi, mode=same_as)
+    for k in ("o_r", "lse_r"):
+        assert np.array_equal(a[k], m[k]), k
