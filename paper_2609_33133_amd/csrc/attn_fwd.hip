@@ -13,14 +13,16 @@
 // Q^T held in registers), the online-softmax update in fp32 with exp2 (the
 // output is rescaled only when a row maximum grows), and 16 MFMAs for
 // O^T += V^T P^T (V^T by transpose reads of the row-major V tile, P^T straight
-// from the S^T accumulators rounded to bf16). LDS addresses come from
-// per-lane offset tables computed once, and the operand reads run a few
-// MFMAs ahead of their MFMA. K and V tiles are double-buffered in LDS
-// (separate arrays, loop unrolled by two, so the compiler can tell the buffer
-// being filled from the one being read) and copied there directly from
-// global memory one block ahead (buffer_load ... lds), so no registers hold
-// staged data. Two workgroups share a CU (two wavefronts per SIMD).
-// The query heads of one KV head run on one XCD (shared K/V in its L2).
+// from the S^T accumulators rounded to bf16). The loop is software-pipelined:
+// the S MFMAs of block b + 1 are interleaved one by one with the exponentials
+// of block b (explicit scheduling groups), so one wavefront keeps the matrix
+// cores and the vector ALUs busy together. LDS addresses come from per-lane
+// offset tables computed once, and operand reads run a few MFMAs ahead of
+// their MFMA. K and V tiles are double-buffered in LDS (separate arrays, loop
+// unrolled by two, so the compiler can tell the buffer being filled from the
+// one being read) and copied there directly from global memory
+// (buffer_load ... lds), so no registers hold staged data. Two workgroups
+// share a CU (two wavefronts per SIMD).
 #include "common.h"
 #include "kernels.h"
 
@@ -31,6 +33,8 @@ namespace {
 constexpr int BM = 128;  // query rows per workgroup
 constexpr int BN = 64;   // keys per block
 constexpr int FWD_DEPTH = 4;  // LDS operand reads run this many MFMAs ahead
+constexpr int PV_DEPTH = 3;   // the same for the P V MFMAs (two reads each)
+constexpr int FWD_VALU_PER_MFMA = 7;  // softmax instructions placed after each S MFMA
 
 template <int D, bool OUT32>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
@@ -72,95 +76,131 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
   TileCopy<BN, D, 4> cp;
   cp.init(kvstride);
-  auto load_block = [&](int b, __bf16* kd, __bf16* vd) {
+  auto load = [&](int b, bool val, __bf16* dst) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
     const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
-    const int nvalid = min(BN, len - kb0);
-    cp.issue(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
-    cp.issue(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
+    const uint16_t* src = val ? (isB ? p.vb : p.va) : (isB ? p.kb : p.ka);
+    cp.issue(dst, src, row0, min(BN, len - kb0), kvstride, kvh * D);
   };
 
   RowOffsets<D> k_off;  // K row l32; row 32 + l32 has the same swizzle, 32 rows further
   k_off.init(l32, hf);
   TrOffsets<D> vtr_off;  // V^T operands
   vtr_off.init(0, lane);
-  auto compute = [&](int b, const __bf16* kl, const __bf16* vl) {
-    const bool isB = b >= nA;
-    const int kb0 = (isB ? b - nA : b) * BN;
-    const int len = isB ? t.b_len : t.a_len;
-    const int qpos_lo = t.b_qpos + wave * 32;  // causal: the wavefront's first query position
-    const bool skip = isB && (kb0 > qpos_lo + 31);
-    if (!skip) {
-      f32x16 s0, s1;
+  const int qpos_lo = t.b_qpos + wave * 32;  // causal: the wavefront's first query position
+
+  // a causal block whose keys all follow the wavefront's queries (and every
+  // later block) contributes nothing
+  auto skipped = [&](int b) { return b >= nA && (b - nA) * BN > qpos_lo + 31; };
+
+  // S^T of one 64-key block (two 32-key halves), raw scores
+  auto s_mfma = [&](const __bf16* kl, f32x16& s0, f32x16& s1) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; }
+    for (int i = 0; i < 16; ++i) { s0[i] = 0.f; s1[i] = 0.f; }
 #pragma unroll
-      for (int ks = 0; ks < D / 16; ++ks) {
-        s0 = mfma32(lds_row8_at<D>(kl, k_off.o[ks]), qreg[ks], s0);
-        s1 = mfma32(lds_row8_at<D>(kl + 32 * D, k_off.o[ks]), qreg[ks], s1);
-      }
-      pace_lds_mfma<D / 8, 1, FWD_DEPTH>();
-      const bool need_mask = (kb0 + BN > len) || (isB && (kb0 + BN - 1 > qpos_lo));
-      if (need_mask) {
-        const int qpos = t.b_qpos + qi;
-#pragma unroll
-        for (int i = 0; i < 16; ++i) {
-          const int k0 = kb0 + acc_row(i, hf);
-          const int k1 = k0 + 32;
-          if ((k0 >= len) || (isB && k0 > qpos)) s0[i] = -INFINITY;
-          if ((k1 >= len) || (isB && k1 > qpos)) s1[i] = -INFINITY;
-        }
-      }
-      float mx = -INFINITY;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
-      mx = fmaxf(mx, __shfl_xor(mx, 32));
-      const float mnew = fmaxf(m_run, mx);
-      if (__any(mnew > m_run)) {
-        // rescale only when some row maximum of this wavefront grew
-        const float alpha = (mnew == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run - mnew) * c);
-        l_run *= alpha;
-#pragma unroll
-        for (int db = 0; db < D / 32; ++db)
-#pragma unroll
-          for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
-        m_run = mnew;
-      }
-      const float ms = (m_run == -INFINITY) ? 0.f : m_run * c;
-      float lsum = 0.f;
-#pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        s0[i] = __builtin_amdgcn_exp2f(s0[i] * c - ms);
-        s1[i] = __builtin_amdgcn_exp2f(s1[i] * c - ms);
-        lsum += s0[i] + s1[i];
-      }
-      l_run += lsum;
-      const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
-      const bf16x8 pb2 = to_bf16x8(s1, 0), pb3 = to_bf16x8(s1, 8);
-#pragma unroll
-      for (int db = 0; db < D / 32; ++db) {
-        oacc[db] = mfma32(vtr_off.read(vl, 0, db), pb0, oacc[db]);
-        oacc[db] = mfma32(vtr_off.read(vl, 1, db), pb1, oacc[db]);
-        oacc[db] = mfma32(vtr_off.read(vl, 2, db), pb2, oacc[db]);
-        oacc[db] = mfma32(vtr_off.read(vl, 3, db), pb3, oacc[db]);
-      }
-      pace_lds_mfma<D / 8, 2, FWD_DEPTH>();
+    for (int ks = 0; ks < D / 16; ++ks) {
+      s0 = mfma32(lds_row8_at<D>(kl, k_off.o[ks]), qreg[ks], s0);
+      s1 = mfma32(lds_row8_at<D>(kl + 32 * D, k_off.o[ks]), qreg[ks], s1);
     }
   };
 
-  if (nblk > 0) load_block(0, k_buf0, v_buf0);
+  // mask, running max and (when it grew) rescale for block b; returns the
+  // exponent offset of the block
+  auto stats = [&](int b, f32x16& s0, f32x16& s1) -> float {
+    const bool isB = b >= nA;
+    const int kb0 = (isB ? b - nA : b) * BN;
+    const int len = isB ? t.b_len : t.a_len;
+    if ((kb0 + BN > len) || (isB && (kb0 + BN - 1 > qpos_lo))) {
+      const int lim = min(len - 1, isB ? t.b_qpos + qi : len - 1) - kb0;  // last visible key of the block
+#pragma unroll
+      for (int i = 0; i < 16; ++i) {
+        if (acc_row(i, hf) > lim) s0[i] = -INFINITY;
+        if (acc_row(i, hf) + 32 > lim) s1[i] = -INFINITY;
+      }
+    }
+    float mx = -INFINITY;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
+    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    const float mnew = fmaxf(m_run, mx);
+    if (__any(mnew > m_run)) {
+      // rescale only when some row maximum of this wavefront grew
+      const float alpha = (mnew == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run - mnew) * c);
+      l_run *= alpha;
+#pragma unroll
+      for (int db = 0; db < D / 32; ++db)
+#pragma unroll
+        for (int i = 0; i < 16; ++i) oacc[db][i] *= alpha;
+      m_run = mnew;
+    }
+    return (m_run == -INFINITY) ? 0.f : m_run * c;
+  };
+
+  // One block step. Scores S(b) arrive in s0/s1 (computed one step earlier);
+  // the S MFMAs of block b + 1 (from kn, into n0/n1) are interleaved one by
+  // one with the exponentials, row sums and bf16 conversion of block b, so the
+  // matrix cores and the vector ALUs of the wavefront work at the same time;
+  // then O += V(b)^T P(b)^T. On the last block the extra S is computed from a
+  // stale buffer and never used.
+  auto step = [&](int b, f32x16& s0, f32x16& s1, const __bf16* kn, const __bf16* vl, f32x16& n0, f32x16& n1) {
+    const float ms = stats(b, s0, s1);
+    __builtin_amdgcn_sched_barrier(0);
+    s_mfma(kn, n0, n1);
+    float lsum = 0.f;
+#pragma unroll
+    for (int i = 0; i < 16; ++i) {
+      s0[i] = __builtin_amdgcn_exp2f(s0[i] * c - ms);
+      s1[i] = __builtin_amdgcn_exp2f(s1[i] * c - ms);
+      lsum += s0[i] + s1[i];
+    }
+    l_run += lsum;
+    const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
+    const bf16x8 pb2 = to_bf16x8(s1, 0), pb3 = to_bf16x8(s1, 8);
+    // 16 MFMAs with one K read each (reads run FWD_DEPTH ahead), the ~112
+    // vector instructions of the softmax spread over them
+    __builtin_amdgcn_sched_group_barrier(0x100, FWD_DEPTH, 0);
+#pragma unroll
+    for (int i = 0; i < D / 8; ++i) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      if (i < D / 8 - FWD_DEPTH) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x402, FWD_VALU_PER_MFMA, 0);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) {
+      oacc[db] = mfma32(vtr_off.read(vl, 0, db), pb0, oacc[db]);
+      oacc[db] = mfma32(vtr_off.read(vl, 1, db), pb1, oacc[db]);
+      oacc[db] = mfma32(vtr_off.read(vl, 2, db), pb2, oacc[db]);
+      oacc[db] = mfma32(vtr_off.read(vl, 3, db), pb3, oacc[db]);
+    }
+    pace_lds_mfma<D / 8, 2, PV_DEPTH>();
+  };
+
+  // K(b + 1) and V(b) are resident while block b is processed; iteration b
+  // loads K(b + 2) over K(b) and V(b + 1) over V(b - 1).
+  f32x16 sa0, sa1, sb0, sb1;
+  if (nblk > 0) {
+    load(0, false, k_buf0);
+    load(0, true, v_buf0);
+    if (nblk > 1) load(1, false, k_buf1);
+  }
   wait_vmem();
   __syncthreads();
+  s_mfma(k_buf0, sa0, sa1);
+  pace_lds_mfma<D / 8, 1, FWD_DEPTH>();
+  __syncthreads();
   for (int b = 0; b < nblk; b += 2) {
-    if (b + 1 < nblk) load_block(b + 1, k_buf1, v_buf1);
-    compute(b, k_buf0, v_buf0);
+    if (b + 2 < nblk) load(b + 2, false, k_buf0);
+    if (b + 1 < nblk) load(b + 1, true, v_buf1);
+    if (!skipped(b)) step(b, sa0, sa1, k_buf1, v_buf0, sb0, sb1);
     wait_vmem();
     __syncthreads();
     if (b + 1 < nblk) {
-      if (b + 2 < nblk) load_block(b + 2, k_buf0, v_buf0);
-      compute(b + 1, k_buf1, v_buf1);
+      if (b + 3 < nblk) load(b + 3, false, k_buf1);
+      if (b + 2 < nblk) load(b + 2, true, v_buf0);
+      if (!skipped(b + 1)) step(b + 1, sb0, sb1, k_buf0, v_buf1, sa0, sa1);
       wait_vmem();
       __syncthreads();
     }
