@@ -120,10 +120,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
         if (acc_row(i, hf) + 32 > lim) s1[i] = -INFINITY;
       }
     }
-    float mx = -INFINITY;
+    // four independent max chains, then a tree (short dependency chains),
+    // and the half-wave exchange without LDS
+    float m4[4];
 #pragma unroll
-    for (int i = 0; i < 16; ++i) mx = fmaxf(mx, fmaxf(s0[i], s1[i]));
-    mx = fmaxf(mx, __shfl_xor(mx, 32));
+    for (int j = 0; j < 4; ++j) m4[j] = fmaxf(s0[j], s1[j]);
+#pragma unroll
+    for (int i = 4; i < 16; ++i) m4[i & 3] = fmaxf(m4[i & 3], fmaxf(s0[i], s1[i]));
+    const float mx = pair_max(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
     const float mnew = fmaxf(m_run, mx);
     if (__any(mnew > m_run)) {
       // rescale only when some row maximum of this wavefront grew
@@ -148,14 +152,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     const float ms = stats(b, s0, s1);
     __builtin_amdgcn_sched_barrier(0);
     s_mfma(kn, n0, n1);
-    float lsum = 0.f;
+    float l4[4] = {0.f, 0.f, 0.f, 0.f};  // four independent partial sums
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       s0[i] = __builtin_amdgcn_exp2f(s0[i] * c - ms);
       s1[i] = __builtin_amdgcn_exp2f(s1[i] * c - ms);
-      lsum += s0[i] + s1[i];
+      l4[i & 3] += s0[i] + s1[i];
     }
-    l_run += lsum;
+    l_run += (l4[0] + l4[1]) + (l4[2] + l4[3]);
     const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
     const bf16x8 pb2 = to_bf16x8(s1, 0), pb3 = to_bf16x8(s1, 8);
     // 16 MFMAs with one K read each (reads run FWD_DEPTH ahead), the ~112
@@ -206,7 +210,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     }
   }
 
-  const float l_tot = l_run + __shfl_xor(l_run, 32);
+  const float l_tot = pair_sum(l_run);
   if (qvalid) {
     const float inv = 1.f / l_tot;
     const int64_t obase = qrow * qstride + head * D;

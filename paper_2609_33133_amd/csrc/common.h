@@ -209,6 +209,20 @@ __device__ __forceinline__ void pace_lds_mfma() {
   __builtin_amdgcn_sched_group_barrier(0x008, DP, 0);
 }
 
+// max / sum of a value and the one of lane l ^ 32, without LDS: after
+// v_permlane32_swap of (x, x) the two results hold, in every lane, x of the
+// lane and x of its partner (in one order or the other). An LDS shuffle
+// (ds_bpermute) costs an LDS round trip and waits for the wavefront's
+// earlier LDS reads.
+__device__ __forceinline__ float pair_max(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float pair_sum(float x) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 // ---------------------------------------------------------------------------- workgroup order
 
 // Workgroups are dispatched round-robin over the 8 XCDs (id % 8), each with
