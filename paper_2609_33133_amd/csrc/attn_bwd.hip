@@ -57,7 +57,9 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
       doreg[ks] = as_bf16x8(qvalid ? ldg16(p.dout + off + ks * 16) : make_uint4(0, 0, 0, 0));
     }
   }
-  const float lse2 = qvalid ? p.lse[(int64_t)head * p.lse_rows + qrow] * kLog2e : 0.f;
+  // S and dP accumulators start at -LSE / scale and -D of this lane's query,
+  // so the MFMAs leave S - LSE / scale and dP - D: P = exp2(c * s), dS = P * dp
+  const float nlse = qvalid ? -p.lse[(int64_t)head * p.lse_rows + qrow] / p.scale : 0.f;
   const float dsq = qvalid ? p.dsum[(int64_t)head * p.lse_rows + qrow] : 0.f;
   const float c = p.scale_log2;
 
@@ -101,7 +103,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
       if (skip) continue;
       f32x16 s, dp;
 #pragma unroll
-      for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
+      for (int i = 0; i < 16; ++i) { s[i] = nlse; dp[i] = -dsq; }
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
         const int o = half ? r1_off.o[ks] : r0_off.o[ks];
@@ -112,12 +114,12 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
       const bool need_mask = (k0 + 32 > len) || (isB && (k0 + 31 > qpos_lo));
 #pragma unroll
       for (int i = 0; i < 16; ++i) {
-        float a = s[i] * c - lse2;
+        float a = s[i] * c;
         if (need_mask) {
           const int kk = k0 + acc_row(i, hf);
           if ((kk >= len) || (isB && kk > qpos)) a = -INFINITY;
         }
-        s[i] = __builtin_amdgcn_exp2f(a) * (dp[i] - dsq);
+        s[i] = __builtin_amdgcn_exp2f(a) * dp[i];
       }
       const bf16x8 g0 = to_bf16x8(s, 0), g1 = to_bf16x8(s, 8);
 #pragma unroll
