@@ -268,20 +268,22 @@ class KernelTimer:
 
 
 def time_steps(fn, steps: int, warmup: int):
+    """Mean ms per step over `steps` back-to-back steps between two events,
+    host wall ms per step, and the per-step times (an event between steps)."""
     import torch
     for _ in range(warmup):
         fn()
     torch.cuda.synchronize()
-    start = torch.cuda.Event(enable_timing=True)
-    end = torch.cuda.Event(enable_timing=True)
+    ev = [torch.cuda.Event(enable_timing=True) for _ in range(steps + 1)]
     t0 = time.perf_counter()
-    start.record()
-    for _ in range(steps):
+    ev[0].record()
+    for i in range(steps):
         fn()
-    end.record()
+        ev[i + 1].record()
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    return start.elapsed_time(end) / steps, wall / steps * 1e3
+    per = [ev[i].elapsed_time(ev[i + 1]) for i in range(steps)]
+    return ev[0].elapsed_time(ev[steps]) / steps, wall / steps * 1e3, per
 
 
 def cpu_baseline(gi, shared_flops: float):
@@ -376,7 +378,7 @@ def main():
     counted = 14.0 * s.head_dim * s.num_q_heads * vp["shared"]
 
     print("[bench] shared path", file=sys.stderr, flush=True)
-    ms, wall_ms = time_steps(lambda: step.run(x), args.steps, args.warmup)
+    ms, wall_ms, per_step = time_steps(lambda: step.run(x), args.steps, args.warmup)
     tflops = counted / (ms * 1e-3) / 1e12
 
     # per-kernel durations over the same number of steps
@@ -431,7 +433,7 @@ def main():
         torch.cuda.empty_cache()
         fstep = FlattenedStep(b, "cuda:0")
         fstep.materialize(x)
-        flat_ms, _ = time_steps(fstep.run, args.steps, args.warmup)
+        flat_ms, _, _ = time_steps(fstep.run, args.steps, args.warmup)
         del fstep
         torch.cuda.empty_cache()
 
@@ -451,6 +453,10 @@ def main():
         "speedup_vs_flattened": None if flat_ms is None else round(flat_ms / ms, 3),
         "flattened_ms_per_step": None if flat_ms is None else round(flat_ms, 4),
         "host_wall_ms_per_step": round(wall_ms, 4),
+        "step_ms": {"median": round(float(np.median(per_step)), 4), "min": round(float(np.min(per_step)), 4),
+                    "max": round(float(np.max(per_step)), 4)},
+        # the same time with the no-recompute convention 12 * d * Hq * valid_pairs
+        "tflops_12d": round(tflops * 12.0 / 14.0, 2),
         "roofline": roof,
         "kernels": kernel_table,
         # time per step of each step of the method (prefill vs replay), from the per-launch events
