@@ -200,6 +200,50 @@ def summarize_pmc(d: str, workload: str) -> str:
     return "\n".join(lines)
 
 
+def summarize_counters(d: str) -> str:
+    """Markdown table per kernel: MFMA busy % (SQ_VALU_MFMA_BUSY_CYCLES over
+    GRBM_GUI_ACTIVE / 8 x 1024 SIMDs, pass d/sq) and achieved HBM read / write
+    GB/s (copy-calibrated FETCH_SIZE / WRITE_SIZE over the dispatch time,
+    passes d/{fetch,write,cfetch,cwrite})."""
+    def load(sub):
+        rows = {}
+        with open(os.path.join(d, sub, "run_counter_collection.csv")) as f:
+            for r in csv.DictReader(f):
+                e = rows.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"]})
+                e[r["Counter_Name"]] = float(r["Counter_Value"])
+                e["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
+        return rows
+    cf = max(e["FETCH_SIZE"] for e in load("cfetch").values())
+    cw = max(e["WRITE_SIZE"] for e in load("cwrite").values())
+    f_scale, w_scale = (1 << 30) / (cf * 1024.0), (1 << 30) / (cw * 1024.0)
+    acc = {}
+    for sub in ("sq", "fetch", "write"):
+        for e in load(sub).values():
+            k = bench_kernel_name(e["name"])
+            if k is None:
+                continue
+            a = acc.setdefault(k, {"sq_ns": 0, "busy": 0.0, "gui": 0.0, "f_ns": 0, "fb": 0.0, "w_ns": 0, "wb": 0.0,
+                                   "n": 0})
+            if sub == "sq":
+                a["busy"] += e["SQ_VALU_MFMA_BUSY_CYCLES"]
+                a["gui"] += e["GRBM_GUI_ACTIVE"] / 8.0 * 1024.0
+                a["sq_ns"] += e["ns"]
+                a["n"] += 1
+            elif sub == "fetch":
+                a["fb"] += e["FETCH_SIZE"] * 1024.0 * f_scale
+                a["f_ns"] += e["ns"]
+            else:
+                a["wb"] += e["WRITE_SIZE"] * 1024.0 * w_scale
+                a["w_ns"] += e["ns"]
+    lines = ["| kernel | launches | avg ms | MFMA busy % | HBM read GB/s | HBM write GB/s |", "|---|---|---|---|---|---|"]
+    for k, a in sorted(acc.items(), key=lambda kv: -kv[1]["sq_ns"]):
+        busy = 100.0 * a["busy"] / a["gui"] if a["gui"] else 0.0
+        rd = a["fb"] / a["f_ns"] if a["f_ns"] else 0.0
+        wr = a["wb"] / a["w_ns"] if a["w_ns"] else 0.0
+        lines.append(f"| {k} | {a['n']} | {a['sq_ns'] / max(a['n'], 1) / 1e6:.3f} | {busy:.1f} | {rd:.0f} | {wr:.0f} |")
+    return "\n".join(lines)
+
+
 def summarize_trace(stats_csv: str) -> str:
     """Markdown table of a rocprofv3 --kernel-trace --stats kernel_stats.csv."""
     lines = ["| kernel | calls | total ms | avg ms | % |", "|---|---|---|---|---|"]
@@ -330,6 +374,9 @@ def main():
     ap.add_argument("--summarize-pmc", default=None, metavar="DIR",
                     help="print the HBM traffic summary of rocprofv3 counter passes in DIR/{fetch,write,cfetch,cwrite} "
                          "(no GPU needed) and exit")
+    ap.add_argument("--summarize-counters", default=None, metavar="DIR",
+                    help="print MFMA busy %% and achieved HBM GB/s per kernel from rocprofv3 counter passes in "
+                         "DIR/{sq,fetch,write,cfetch,cwrite} (no GPU needed) and exit")
     ap.add_argument("--summarize-trace", default=None, metavar="CSV",
                     help="print a table of a rocprofv3 kernel_stats.csv (no GPU needed) and exit")
     ap.add_argument("--copy-calibration", action="store_true",
@@ -337,6 +384,9 @@ def main():
     args = ap.parse_args()
     if args.summarize_pmc:
         print(summarize_pmc(args.summarize_pmc, args.workload))
+        return
+    if args.summarize_counters:
+        print(summarize_counters(args.summarize_counters))
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))

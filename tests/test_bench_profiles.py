@@ -75,3 +75,27 @@ def test_trace_summary(tmp_path):
                     1000000.0, 100.0, 1, 2, 0])
     md = bench.summarize_trace(str(p))
     assert "| attn_dq_kernel<128> | 4 | 4.00 | 1.0000 | 100.00 |" in md
+
+
+def test_counter_summary_busy_and_bandwidth(tmp_path):
+    d = str(tmp_path)
+    fields = FIELDS + ["Start_Timestamp", "End_Timestamp"]
+    k = "void augtree::(anonymous namespace)::lse_merge_kernel(augtree::MergeParams)"
+
+    def wr(sub, rows):
+        os.makedirs(f"{d}/{sub}", exist_ok=True)
+        with open(f"{d}/{sub}/run_counter_collection.csv", "w", newline="") as f:
+            w = csv.DictWriter(f, fieldnames=fields)
+            w.writeheader()
+            for r in rows:
+                w.writerow(dict(zip(fields, r)))
+
+    wr("cfetch", [(1, "copy", "FETCH_SIZE", 1 << 19, 0, 1)])
+    wr("cwrite", [(1, "copy", "WRITE_SIZE", 1 << 20, 0, 1)])
+    # one launch of 1 us: 1000 KiB fetch counter -> 2 * 1000 KiB read; 500 KiB written
+    wr("fetch", [(1, k, "FETCH_SIZE", 1000.0, 0, 1000)])
+    wr("write", [(1, k, "WRITE_SIZE", 500.0, 0, 1000)])
+    # 8 XCDs x 100 cycles -> 100 cycles x 1024 SIMDs; 25600 busy SIMD-cycles = 25 %
+    wr("sq", [(1, k, "SQ_VALU_MFMA_BUSY_CYCLES", 25600.0, 0, 1000), (1, k, "GRBM_GUI_ACTIVE", 800.0, 0, 1000)])
+    md = bench.summarize_counters(d)
+    assert "| lse_merge_kernel | 1 | 0.001 | 25.0 | 2048 | 512 |" in md
