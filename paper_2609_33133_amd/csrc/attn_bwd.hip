@@ -177,11 +177,11 @@ constexpr int DKV_DEPTH = 3;  // LDS operand reads run this many MFMAs ahead
 template <int D, bool OUT32>
 __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   // the workgroup's K and V tiles (operands of S = Q K^T and dP = dO V^T);
-  // query blocks double-buffered in separate arrays; lse2 = LSE * log2(e),
-  // +inf past the end of the range
+  // query blocks double-buffered in separate arrays, with -LSE / scale and
+  // -D of their rows
   __shared__ __bf16 k_tile[KV_BN * D], v_tile[KV_BN * D];
   __shared__ __bf16 q_buf0[KV_BQ * D], q_buf1[KV_BQ * D], o_buf0[KV_BQ * D], o_buf1[KV_BQ * D];
-  __shared__ float lse2_buf0[KV_BQ], lse2_buf1[KV_BQ], dsum_buf0[KV_BQ], dsum_buf1[KV_BQ];
+  __shared__ float nlse_buf0[KV_BQ], nlse_buf1[KV_BQ], ndsum_buf0[KV_BQ], ndsum_buf1[KV_BQ];
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
   const int kq = wave & 3;   // 32-key slice of the tile
   const int qs = wave >> 2;  // 32-row half of every query block
@@ -237,9 +237,12 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
       stat_n = nvalid;
     }
   };
+  // stored as the S and dP accumulator start values -LSE / scale and -D
+  // (-inf past the end of the range, so those rows get P = 0)
+  const float neg_inv_scale = -1.f / p.scale;
   auto store_stat = [&](float* ld, float* dd) {
-    if (wave_u == 0) ld[lane] = lane < stat_n ? stat * kLog2e : INFINITY;
-    else if (wave_u == 1) dd[lane] = lane < stat_n ? stat : 0.f;
+    if (wave_u == 0) ld[lane] = lane < stat_n ? stat * neg_inv_scale : -INFINITY;
+    else if (wave_u == 1) dd[lane] = lane < stat_n ? -stat : 0.f;
   };
 
   const int key_pos = t.kpos0 + kj;  // this lane's key position (causal tiles)
@@ -254,9 +257,21 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     const bool skip = t.causal && (qpos0 + 31 < t.kpos0 + kw0);
     if (skip) return;
     const bool need_mask = t.causal && (qpos0 < t.kpos0 + kw0 + 31);
+    // S and dP accumulators start at -LSE / scale and -D of their rows
+    // (register i holds row g4 * 8 + 4 * hf + e, i = 4 * g4 + e), so the
+    // MFMAs leave S - LSE / scale and dP - D: P = exp2(c * s), dS = P * dp.
+    // The start values are read in a scheduling region of their own: in the
+    // paced region below they would take the first operand-read slots.
     f32x16 s, dp;
 #pragma unroll
-    for (int i = 0; i < 16; ++i) { s[i] = 0.f; dp[i] = 0.f; }
+    for (int g4 = 0; g4 < 4; ++g4) {
+      const int r0 = qs * 32 + g4 * 8 + hf * 4;
+      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lsel[r0]);
+      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dsl[r0]);
+#pragma unroll
+      for (int e = 0; e < 4; ++e) { s[g4 * 4 + e] = l4[e]; dp[g4 * 4 + e] = d4[e]; }
+    }
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
       s = mfma32(lds_row8_at<D>(ql, qrow_off.o[ks]), lds_row8_at<D>(k_tile, key_off.o[ks]), s);
@@ -264,22 +279,16 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     }
     pace_lds_mfma<D / 8, 2, DKV_DEPTH>();
 #pragma unroll
-    for (int g4 = 0; g4 < 4; ++g4) {
-      const int r0 = qs * 32 + g4 * 8 + hf * 4;
-      const f32x4 l4 = *reinterpret_cast<const f32x4*>(&lsel[r0]);
-      const f32x4 d4 = *reinterpret_cast<const f32x4*>(&dsl[r0]);
-#pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        const int i = g4 * 4 + e;
-        float a = s[i] * c - l4[e];
-        if (need_mask && key_pos > qpos0 + g4 * 8 + hf * 4 + e) a = -INFINITY;
-        const float pr = __builtin_amdgcn_exp2f(a);
-        s[i] = pr;
-        dp[i] = pr * (dp[i] - d4[e]);
-      }
+    for (int i = 0; i < 16; ++i) {
+      float a = s[i] * c;
+      if (need_mask && key_pos > qpos0 + acc_row(i, hf)) a = -INFINITY;
+      const float pr = __builtin_amdgcn_exp2f(a);
+      s[i] = pr;
+      dp[i] = pr * dp[i];
     }
     const bf16x8 pb0 = to_bf16x8(s, 0), pb1 = to_bf16x8(s, 8);
     const bf16x8 gb0 = to_bf16x8(dp, 0), gb1 = to_bf16x8(dp, 8);
+    __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       dv[db] = mfma32(pb0, qtr_off.read(dl, 0, db), dv[db]);
@@ -292,20 +301,20 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
 
   if (nblk > 0) {
     load_block(0, q_buf0, o_buf0);
-    store_stat(lse2_buf0, dsum_buf0);
+    store_stat(nlse_buf0, ndsum_buf0);
   }
   wait_vmem();
   __syncthreads();
   for (int b = 0; b < nblk; b += 2) {
     if (b + 1 < nblk) load_block(b + 1, q_buf1, o_buf1);
-    compute(b, q_buf0, o_buf0, lse2_buf0, dsum_buf0);
-    if (b + 1 < nblk) store_stat(lse2_buf1, dsum_buf1);
+    compute(b, q_buf0, o_buf0, nlse_buf0, ndsum_buf0);
+    if (b + 1 < nblk) store_stat(nlse_buf1, ndsum_buf1);
     wait_vmem();
     __syncthreads();
     if (b + 1 < nblk) {
       if (b + 2 < nblk) load_block(b + 2, q_buf0, o_buf0);
-      compute(b + 1, q_buf1, o_buf1, lse2_buf1, dsum_buf1);
-      if (b + 2 < nblk) store_stat(lse2_buf0, dsum_buf0);
+      compute(b + 1, q_buf1, o_buf1, nlse_buf1, ndsum_buf1);
+      if (b + 2 < nblk) store_stat(nlse_buf0, ndsum_buf0);
       wait_vmem();
       __syncthreads();
     }
