@@ -172,7 +172,8 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 
 constexpr int KV_BN = 128;  // keys per workgroup (32 per wavefront pair)
 constexpr int KV_BQ = 64;   // query rows per block (32 per wavefront of a pair)
-constexpr int DKV_DEPTH = 3;  // LDS operand reads run this many MFMAs ahead
+constexpr int DKV_SDP_DEPTH = 2;  // LDS operand reads of S / dP run this many MFMAs ahead
+constexpr int DKV_DVK_DEPTH = 2;  // the same for the dV / dK transpose reads
 
 template <int D, bool OUT32>
 __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
@@ -182,9 +183,10 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   __shared__ __bf16 k_tile[KV_BN * D], v_tile[KV_BN * D];
   __shared__ __bf16 q_buf0[KV_BQ * D], q_buf1[KV_BQ * D], o_buf0[KV_BQ * D], o_buf1[KV_BQ * D];
   __shared__ float nlse_buf0[KV_BQ], nlse_buf1[KV_BQ], ndsum_buf0[KV_BQ], ndsum_buf1[KV_BQ];
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
-  const int kq = wave & 3;   // 32-key slice of the tile
-  const int qs = wave >> 2;  // 32-row half of every query block
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
+  const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches below
+  const int kq = wave_u & 3;   // 32-key slice of the tile
+  const int qs = wave_u >> 2;  // 32-row half of every query block
   const int tile_id = blockIdx.x / p.hkv;
   const int kvh = blockIdx.x - tile_id * p.hkv;
   const KVTile t = p.tiles[tile_id];
@@ -214,7 +216,6 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   // query block into `stat`; they are scaled and stored to LDS at the end of
   // the iteration, so nothing waits on these loads (or on the tile copies
   // issued before them) while the current block is computed.
-  const int wave_u = __builtin_amdgcn_readfirstlane(wave);
   float stat = 0.f;
   int stat_n = 0;
   TileCopy<KV_BQ, D, 8> qc;
@@ -277,12 +278,15 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
       s = mfma32(lds_row8_at<D>(ql, qrow_off.o[ks]), lds_row8_at<D>(k_tile, key_off.o[ks]), s);
       dp = mfma32(lds_row8_at<D>(dl, qrow_off.o[ks]), lds_row8_at<D>(v_tile, key_off.o[ks]), dp);
     }
-    pace_lds_mfma<D / 8, 2, DKV_DEPTH>();
+    pace_lds_mfma<D / 8, 2, DKV_SDP_DEPTH>();
+    if (need_mask) {  // only blocks that cross the diagonal
+#pragma unroll
+      for (int i = 0; i < 16; ++i)
+        if (key_pos > qpos0 + acc_row(i, hf)) s[i] = -INFINITY;
+    }
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
-      float a = s[i] * c;
-      if (need_mask && key_pos > qpos0 + acc_row(i, hf)) a = -INFINITY;
-      const float pr = __builtin_amdgcn_exp2f(a);
+      const float pr = __builtin_amdgcn_exp2f(s[i] * c);
       s[i] = pr;
       dp[i] = pr * dp[i];
     }
@@ -296,7 +300,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
       dk[db] = mfma32(gb0, qtr_off.read(ql, 0, db), dk[db]);
       dk[db] = mfma32(gb1, qtr_off.read(ql, 1, db), dk[db]);
     }
-    pace_lds_mfma<D / 8, 2, DKV_DEPTH>();
+    pace_lds_mfma<D / 8, 2, DKV_DVK_DEPTH>();
   };
 
   if (nblk > 0) {
