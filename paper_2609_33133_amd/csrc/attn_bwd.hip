@@ -111,16 +111,17 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
         dp = mfma32(lds_row8_at<D>(vl, o), doreg[ks], dp);
       }
       pace_lds_mfma<D / 8, 1, DQ_DEPTH>();
-      const bool need_mask = (k0 + 32 > len) || (isB && (k0 + 31 > qpos_lo));
+      // ragged end or diagonal; the condition is uniform over the wavefront
+      // (a scalar branch)
+      if (__builtin_amdgcn_readfirstlane((k0 + 32 > len) || (isB && (k0 + 31 > qpos_lo)))) {
 #pragma unroll
-      for (int i = 0; i < 16; ++i) {
-        float a = s[i] * c;
-        if (need_mask) {
+        for (int i = 0; i < 16; ++i) {
           const int kk = k0 + acc_row(i, hf);
-          if ((kk >= len) || (isB && kk > qpos)) a = -INFINITY;
+          if ((kk >= len) || (isB && kk > qpos)) s[i] = -INFINITY;
         }
-        s[i] = __builtin_amdgcn_exp2f(a) * dp[i];
       }
+#pragma unroll
+      for (int i = 0; i < 16; ++i) s[i] = __builtin_amdgcn_exp2f(s[i] * c) * dp[i];
       const bf16x8 g0 = to_bf16x8(s, 0), g1 = to_bf16x8(s, 8);
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
