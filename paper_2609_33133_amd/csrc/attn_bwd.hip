@@ -173,16 +173,25 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 
 constexpr int KV_BN = 128;  // keys per workgroup (32 per wavefront pair)
 constexpr int KV_BQ = 64;   // query rows per block (32 per wavefront of a pair)
-constexpr int DKV_SDP_DEPTH = 2;  // LDS operand reads of S / dP run this many MFMAs ahead
+constexpr int DKV_SDP_DEPTH = 3;  // LDS operand reads of S / dP run this many MFMAs ahead
 constexpr int DKV_DVK_DEPTH = 2;  // the same for the dV / dK transpose reads
 
 template <int D, bool OUT32>
 __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   // the workgroup's K and V tiles (operands of S = Q K^T and dP = dO V^T);
   // query blocks double-buffered in separate arrays, with -LSE / scale and
-  // -D of their rows
-  __shared__ __bf16 k_tile[KV_BN * D], v_tile[KV_BN * D];
-  __shared__ __bf16 q_buf0[KV_BQ * D], q_buf1[KV_BQ * D], o_buf0[KV_BQ * D], o_buf1[KV_BQ * D];
+  // -D of their rows.
+  // The query-block buffers get the larger alignment so that they are placed
+  // first (LDS variables are laid out by alignment, then size): every
+  // address inside them is then below 64 KB, so the buffer base and the 16 B
+  // column steps fold into the 16-bit offset field of the LDS reads and one
+  // register per operand serves all four buffers. The K/V tile above them is
+  // addressed through opaque per-lane addresses (V at an immediate +32 KB).
+  __shared__ __attribute__((aligned(1024))) __bf16 q_buf0[KV_BQ * D], q_buf1[KV_BQ * D], o_buf0[KV_BQ * D],
+      o_buf1[KV_BQ * D];
+  __shared__ __bf16 kv_tile[2 * KV_BN * D];  // K rows, then V rows
+  __bf16* const k_tile = kv_tile;
+  __bf16* const v_tile = kv_tile + KV_BN * D;
   __shared__ float nlse_buf0[KV_BQ], nlse_buf1[KV_BQ], ndsum_buf0[KV_BQ], ndsum_buf1[KV_BQ];
   const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
   const int wave_u = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches below
@@ -251,6 +260,10 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   RowOffsets<D> qrow_off, key_off;   // Q/dO rows of this wave's half; K/V rows of its keys
   qrow_off.init(qs * 32 + l32, hf);
   key_off.init(kj, hf);
+  // LDS addresses of this lane's K rows; the V rows are KV_BN * D * 2 bytes on
+  // (an immediate offset of the same register)
+#pragma unroll
+  for (int ks = 0; ks < D / 16; ++ks) key_off.o[ks] = (int)opaque(lds_addr(k_tile) + key_off.o[ks]);
   TrOffsets<D> qtr_off;              // Q^T / dO^T operands of this wave's half
   qtr_off.init(qs * 32, lane);
   auto compute = [&](int b, const __bf16* ql, const __bf16* dl, const float* lsel, const float* dsl) {
@@ -276,8 +289,8 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      s = mfma32(lds_row8_at<D>(ql, qrow_off.o[ks]), lds_row8_at<D>(k_tile, key_off.o[ks]), s);
-      dp = mfma32(lds_row8_at<D>(dl, qrow_off.o[ks]), lds_row8_at<D>(v_tile, key_off.o[ks]), dp);
+      s = mfma32(lds_row8_at<D>(ql, qrow_off.o[ks]), lds_read16(kv_tile, key_off.o[ks]), s);
+      dp = mfma32(lds_row8_at<D>(dl, qrow_off.o[ks]), lds_read16<KV_BN * D * 2>(kv_tile, key_off.o[ks]), dp);
     }
     pace_lds_mfma<D / 8, 2, DKV_SDP_DEPTH>();
     if (need_mask) {  // only blocks that cross the diagonal

@@ -99,6 +99,35 @@ __device__ __forceinline__ bf16x8 lds_row8_at(const __bf16* tile, int byte_off) 
   return *reinterpret_cast<const bf16x8*>(reinterpret_cast<const char*>(tile) + byte_off);
 }
 
+typedef __attribute__((address_space(3))) const char* lds_cptr;
+
+// Byte address of a __shared__ object inside the workgroup's LDS.
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return (uint32_t)(uintptr_t)(lds_cptr)(const char*)p;
+}
+
+// A value the compiler cannot see through: an LDS address formed as
+// opaque(tile base + per-lane offset) is one register, and reads at fixed
+// distances from it (a second tile 32 KB further on) become immediate
+// offsets of the same register instead of registers of their own. (Without
+// it the compiler folds both tile bases into per-lane constants; above 64 KB
+// they no longer fit the 16-bit offset field.)
+__device__ __forceinline__ uint32_t opaque(uint32_t x) {
+  asm("" : "+v"(x));
+  return x;
+}
+
+// 16-byte read of a __shared__ array `base` at LDS byte address `addr` + IMM
+// (addr = opaque(lds_addr(base) + offset)). The pointer is derived from
+// `base`, so the access keeps that array's alias scope (the wait inserted
+// for in-flight direct-to-LDS copies into other arrays is then not needed),
+// and its address is the register `addr` plus an immediate.
+template <int IMM = 0>
+__device__ __forceinline__ bf16x8 lds_read16(const __bf16* base, uint32_t addr) {
+  const char* b = reinterpret_cast<const char*>(base);
+  return *reinterpret_cast<const bf16x8*>(b + (addr - lds_addr(base)) + IMM);
+}
+
 __device__ __forceinline__ s16x4 lds_tr16(const __bf16* p) {
   return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4*)(p));
 }
