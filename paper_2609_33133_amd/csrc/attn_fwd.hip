@@ -35,6 +35,11 @@ constexpr int BN = 64;   // keys per block
 constexpr int FWD_DEPTH = 4;  // LDS operand reads run this many MFMAs ahead
 constexpr int PV_DEPTH = 3;   // the same for the P V MFMAs (two reads each)
 constexpr int FWD_VALU_PER_MFMA = 7;  // softmax instructions placed after each S MFMA
+// The exponent reference of a row (its running maximum) moves only when a
+// block's maximum exceeds it by more than this many powers of two. Exact: the
+// reference cancels between numerator and denominator; P stays <= 2^8, far
+// inside the fp32 and bf16 ranges.
+constexpr float RESCALE_MARGIN_LOG2 = 8.f;
 
 template <int D, bool OUT32>
 __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
@@ -129,8 +134,10 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     for (int i = 4; i < 16; ++i) m4[i & 3] = fmaxf(m4[i & 3], fmaxf(s0[i], s1[i]));
     const float mx = pair_max(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
     const float mnew = fmaxf(m_run, mx);
-    if (__any(mnew > m_run)) {
-      // rescale only when some row maximum of this wavefront grew
+    // rescale only when some row maximum of this wavefront passed its
+    // reference by more than the margin (always on a row's first visible key:
+    // the reference starts at -inf)
+    if (__any(mx * c > m_run * c + RESCALE_MARGIN_LOG2)) {
       const float alpha = (mnew == -INFINITY) ? 1.f : __builtin_amdgcn_exp2f((m_run - mnew) * c);
       l_run *= alpha;
 #pragma unroll

@@ -100,6 +100,33 @@ def test_q_zero_probe_closed_form():
                 assert rel(got["o_r"][r0:r1, :, 0], want) < 1e-2
 
 
+def test_rising_logits_move_the_softmax_reference():
+    """Logits that rise along the key positions, at a different slope per
+    query head: the running row maximum of the online softmax grows on every
+    64-key block, by steps below and above the forward kernel's rescale
+    margin (2^8), and never (negative slope). The ramp sits in component 0:
+    key j has k[0] = j / 640 and query head h has q[0] = slope_h. (A steeper
+    key ramp with flatter slopes gives the same logits but a large common
+    k[0] over the keys that carry the softmax mass, whose cancellation in
+    dQ = s dS K amplifies the bf16 rounding of dS beyond the tolerance.)"""
+    shape = I.custom_shape([700], [[150, 90]], 8, 2, 128)
+    gi = I.make_inputs(shape, seed=11)
+    P = shape.prompt_lens[0]
+    # log2-unit rise per 64 keys = slope * 64 / 640 * scale * log2(e) ~ 0.01275 * slope
+    slopes = np.array([0.0, 40.0, 160.0, 400.0, 640.0, 1000.0, 1570.0, -300.0], np.float32)
+    gi.q_p[:, :, 0] = I.f32_to_bf16_bits(np.broadcast_to(slopes, (P, 8)).copy())
+    gi.q_r[:, :, 0] = I.f32_to_bf16_bits(np.broadcast_to(slopes, (gi.q_r.shape[0], 8)).copy())
+    gi.k_p[:, :, 0] = I.f32_to_bf16_bits((np.arange(P, dtype=np.float32) / 640)[:, None].repeat(2, 1))
+    for b in range(2):
+        r0, r1 = shape.cu_resp[b], shape.cu_resp[b + 1]
+        pos = (P + np.arange(r1 - r0, dtype=np.float32)) / 640
+        gi.k_r[r0:r1, :, 0] = I.f32_to_bf16_bits(pos[:, None].repeat(2, 1))
+    ref = oracle(gi)
+    for mode in (REPLAY_FUSED, REPLAY_SPLIT):
+        got, _ = run_shared(gi, mode=mode)
+        assert_close(got, ref, f"rising logits mode {mode}")
+
+
 def test_fused_equals_split():
     shape = I.custom_shape([333, 70], [[100, 200], [65, 1, 129]], 8, 2, 128)
     gi = I.make_inputs(shape, seed=8, qk_mult=1.0)
