@@ -104,6 +104,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
       f32x16 s, dp;
 #pragma unroll
       for (int i = 0; i < 16; ++i) { s[i] = nlse; dp[i] = -dsq; }
+      set_wave_priority<0>();
 #pragma unroll
       for (int ks = 0; ks < D / 16; ++ks) {
         const int o = half ? r1_off.o[ks] : r0_off.o[ks];
@@ -111,6 +112,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
         dp = mfma32(lds_row8_at<D>(vl, o), doreg[ks], dp);
       }
       pace_lds_mfma<D / 8, 1, DQ_DEPTH>();
+      set_wave_priority<1>();
       // ragged end or diagonal; the condition is uniform over the wavefront
       // (a scalar branch)
       if (__builtin_amdgcn_readfirstlane((k0 + 32 > len) || (isB && (k0 + 31 > qpos_lo)))) {
@@ -123,12 +125,14 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) s[i] = __builtin_amdgcn_exp2f(s[i] * c) * dp[i];
       const bf16x8 g0 = to_bf16x8(s, 0), g1 = to_bf16x8(s, 8);
+      set_wave_priority<0>();
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
         acc[db] = mfma32(ktr_off.read(kl, 2 * half, db), g0, acc[db]);
         acc[db] = mfma32(ktr_off.read(kl, 2 * half + 1, db), g1, acc[db]);
       }
       pace_lds_mfma<D / 16, 2, DQ_DEPTH>();
+      set_wave_priority<1>();
     }
   };
 
@@ -286,13 +290,14 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
 #pragma unroll
       for (int e = 0; e < 4; ++e) { s[g4 * 4 + e] = l4[e]; dp[g4 * 4 + e] = d4[e]; }
     }
-    __builtin_amdgcn_sched_barrier(0);
+    set_wave_priority<0>();
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
       s = mfma32(lds_row8_at<D>(ql, qrow_off.o[ks]), lds_read16(kv_tile, key_off.o[ks]), s);
       dp = mfma32(lds_row8_at<D>(dl, qrow_off.o[ks]), lds_read16<KV_BN * D * 2>(kv_tile, key_off.o[ks]), dp);
     }
     pace_lds_mfma<D / 8, 2, DKV_SDP_DEPTH>();
+    set_wave_priority<1>();
     if (need_mask) {  // only blocks that cross the diagonal
 #pragma unroll
       for (int i = 0; i < 16; ++i)
@@ -306,7 +311,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     }
     const bf16x8 pb0 = to_bf16x8(s, 0), pb1 = to_bf16x8(s, 8);
     const bf16x8 gb0 = to_bf16x8(dp, 0), gb1 = to_bf16x8(dp, 8);
-    __builtin_amdgcn_sched_barrier(0);
+    set_wave_priority<0>();
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       dv[db] = mfma32(pb0, qtr_off.read(dl, 0, db), dv[db]);
@@ -315,6 +320,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
       dk[db] = mfma32(gb1, qtr_off.read(ql, 1, db), dk[db]);
     }
     pace_lds_mfma<D / 8, 2, DKV_DVK_DEPTH>();
+    set_wave_priority<1>();
   };
 
   if (nblk > 0) {

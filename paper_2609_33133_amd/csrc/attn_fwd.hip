@@ -178,7 +178,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       if (i < D / 8 - FWD_DEPTH) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
       __builtin_amdgcn_sched_group_barrier(0x402, FWD_VALU_PER_MFMA, 0);
     }
-    __builtin_amdgcn_sched_barrier(0);
+    set_wave_priority<1>();
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
       oacc[db] = mfma32(vtr_off.read(vl, 0, db), pb0, oacc[db]);
@@ -187,6 +187,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       oacc[db] = mfma32(vtr_off.read(vl, 3, db), pb3, oacc[db]);
     }
     pace_lds_mfma<D / 8, 2, PV_DEPTH>();
+    set_wave_priority<0>();
   };
 
   // K(b + 1) and V(b) are resident while block b is processed; iteration b

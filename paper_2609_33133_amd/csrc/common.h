@@ -16,8 +16,14 @@
 // transpose read (TrOffsets).
 //
 // LDS tiles are row-major, unpadded, with the 16-byte chunks of row r stored
-// at chunk index (chunk ^ swz(r)): 16-byte row reads of 16 consecutive rows
-// and transpose reads of 4 consecutive rows both touch distinct banks.
+// at chunk index (chunk ^ swz(r)). The LDS has 64 banks of 4 bytes; a 16-byte
+// row read serves 16 lanes per cycle (16 consecutive rows, one chunk each)
+// and a transpose read 32 lanes (4 consecutive rows x 4 chunks, 8 bytes per
+// lane). swz makes both conflict-free: over 16 consecutive rows it is a
+// permutation of the chunk indices, and inside every aligned group of 4 rows
+// it moves each row to a different aligned group of 4 chunks. (A swizzle
+// without the second property makes every transpose read 2-way conflicted;
+// the conflict cycles showed in the LDS counters.)
 #pragma once
 
 #include <hip/hip_runtime.h>
@@ -71,8 +77,10 @@ __device__ __forceinline__ uint32_t half16(const uint4& v, int e) {
 
 template <int D>
 __device__ __forceinline__ int swz(int row) {
-  if constexpr (D == 128) return ((row & 7) << 1) | ((row >> 3) & 1);  // 16 chunks per row
-  else return (row >> 1) & 7;                                            // 8 chunks per row
+  // D = 128: 16 chunks per row, row = 4a + b -> 4b + a
+  if constexpr (D == 128) return ((row & 3) << 2) | ((row >> 2) & 3);
+  // D = 64: 8 chunks per row, two rows per 256-byte bank row; row = 4a + 2b + p -> 4b + a
+  else return (((row >> 1) & 1) << 2) | ((row >> 2) & 3);
 }
 
 // element offset of (row, col) in a swizzled [*, D] tile; col % 4 == 0 keeps
@@ -236,6 +244,19 @@ __device__ __forceinline__ void pace_lds_mfma() {
     __builtin_amdgcn_sched_group_barrier(0x100, R, 0);     // DS reads
   }
   __builtin_amdgcn_sched_group_barrier(0x008, DP, 0);
+}
+
+// Issue priority of the wavefront (s_setprio), fenced so that the compiler
+// keeps the instructions of each phase on their side of the change. With two
+// wavefronts per SIMD, the one that raises its priority is issued first when
+// both are ready: the forward raises it for its PV MFMAs, the backward
+// kernels for everything but their MFMA runs (softmax, block change), which
+// keeps the matrix core fed by one wavefront while the other catches up.
+template <int P>
+__device__ __forceinline__ void set_wave_priority() {
+  __builtin_amdgcn_sched_barrier(0);
+  __builtin_amdgcn_s_setprio(P);
+  __builtin_amdgcn_sched_barrier(0);
 }
 
 // max / sum of a value and the one of lane l ^ 32, without LDS: after
