@@ -1,7 +1,8 @@
 // Host side of libaugtree: argument validation, tile schedules and launches.
 //
 // Every entry point validates its arguments on the host, builds the tile
-// schedule of its kernels from the host offsets (heaviest tiles first, so the
+// schedule of its kernels from the host offsets (segment by segment, heaviest
+// first, so concurrent workgroups share a segment's blocks in L2 and the
 // ragged tail of a launch is made of short tiles), copies the schedule into
 // the caller's workspace on the caller's stream, and enqueues the kernels.
 // Nothing is allocated, nothing is synchronised, no state is kept between
@@ -16,6 +17,7 @@
 #include <cstring>
 #include <numeric>
 #include <string>
+#include <tuple>
 #include <vector>
 
 #include "../../include/augtree.h"
@@ -148,23 +150,62 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
-// heaviest first; ties keep construction order
+int64_t qtile_cost(const QTile& t) { return (int64_t)t.q_len * (t.a_len + t.b_len); }
+int64_t kvtile_cost(const KVTile& t) { return (int64_t)t.q_len * t.kv_len; }
+
+// Tile order. Each XCD runs the tiles of one KV head in list order, so
+// concurrent workgroups share a K/V or Q/dO block in the XCD's L2 only when
+// they work on the same segment (a group's prompt, a branch); a cost-only
+// heaviest-first order mixes the tiles of all segments (16 equal branches:
+// ~2 concurrent tiles per branch). So segments run one after the other, by
+// total cost, each heaviest tile first. A segment's heaviest tile must still
+// start early enough not to end alone: the work listed from the segment's
+// start to the end of the launch has to cover `conc` (the tiles the chip runs
+// at once) times that tile. Segments that fail (the last, small ones; decided
+// from the end backwards) go to a pool at the end of the list, heaviest tile
+// first across the pooled segments.
 template <class T, class F>
-void sort_by_cost(std::vector<T>& v, F cost) {
-  std::vector<std::pair<int64_t, size_t>> key(v.size());
-  for (size_t i = 0; i < v.size(); ++i) key[i] = {-cost(v[i]), i};
-  std::stable_sort(key.begin(), key.end());
+void sort_segment_major(std::vector<T>& v, const std::vector<int>& seg, F cost, int conc) {
+  int nseg = 0;
+  for (int x : seg) nseg = std::max(nseg, x + 1);
+  std::vector<int64_t> total(nseg, 0), top(nseg, 0);
+  for (size_t i = 0; i < v.size(); ++i) {
+    total[seg[i]] += cost(v[i]);
+    top[seg[i]] = std::max(top[seg[i]], cost(v[i]));
+  }
+  std::vector<int> order(nseg);
+  std::iota(order.begin(), order.end(), 0);
+  std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return total[a] > total[b]; });
+  std::vector<int> rank(nseg, 0);
+  std::vector<char> pooled(nseg, 0);
+  int64_t after = 0;  // work listed after the segment being decided
+  for (int k = nseg - 1; k >= 0; --k) {
+    const int g = order[k];
+    rank[g] = k;
+    if (after + total[g] < (int64_t)conc * top[g]) pooled[g] = 1;
+    after += total[g];
+  }
+  std::vector<std::tuple<int, int, int64_t, size_t>> key(v.size());
+  for (size_t i = 0; i < v.size(); ++i) {
+    const int g = seg[i];
+    key[i] = {pooled[g] ? 1 : 0, pooled[g] ? 0 : rank[g], -cost(v[i]), i};
+  }
+  std::sort(key.begin(), key.end());
   std::vector<T> out(v.size());
-  for (size_t i = 0; i < v.size(); ++i) out[i] = v[key[i].second];
+  for (size_t i = 0; i < v.size(); ++i) out[i] = v[std::get<3>(key[i])];
   v.swap(out);
 }
 
-int64_t qtile_cost(const QTile& t) { return (int64_t)t.q_len * (t.a_len + t.b_len); }
-int64_t kvtile_cost(const KVTile& t) { return (int64_t)t.q_len * t.kv_len; }
+// Tiles the chip runs at once (256 CUs of MI355X; a scheduling estimate, not
+// a limit): query tiles take `hq` workgroups, two per CU; key tiles `hkv`
+// workgroups, one per CU.
+int conc_qtiles(const Shape& s) { return std::max(1, 2 * 256 / s.hq); }
+int conc_kvtiles(const Shape& s) { return std::max(1, 256 / s.hkv); }
 
 // prompt causal tiles (prefill fwd and dQ)
 std::vector<QTile> prefill_qtiles(const Shape& s, int bm) {
   std::vector<QTile> v;
+  std::vector<int> seg;
   for (int g = 0; g < s.ng; ++g) {
     const int P = s.cp[g + 1] - s.cp[g];
     for (int t0 = 0; t0 < P; t0 += bm) {
@@ -175,9 +216,10 @@ std::vector<QTile> prefill_qtiles(const Shape& s, int bm) {
       t.b_len = t0 + t.q_len;
       t.b_qpos = t0;
       v.push_back(t);
+      seg.push_back(g);
     }
   }
-  sort_by_cost(v, qtile_cost);
+  sort_segment_major(v, seg, qtile_cost, conc_qtiles(s));
   return v;
 }
 
@@ -188,6 +230,7 @@ enum { RP_PROMPT = 0, RP_OWN = 1, RP_FUSED = 2 };
 // `keep` (optional, one flag per group) limits the tiles to the flagged groups
 std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which, const std::vector<char>* keep = nullptr) {
   std::vector<QTile> v;
+  std::vector<int> seg;  // prompt partial: the group; otherwise the branch
   for (int g = 0; g < s.ng; ++g) {
     if (keep && !(*keep)[g]) continue;
     const int P = s.cp[g + 1] - s.cp[g];
@@ -200,6 +243,7 @@ std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which, const std::v
         t.a_row0 = s.cp[g];
         t.a_len = P;
         v.push_back(t);
+        seg.push_back(g);
       }
       continue;
     }
@@ -217,10 +261,11 @@ std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which, const std::v
         t.b_len = t0 + t.q_len;
         t.b_qpos = t0;
         v.push_back(t);
+        seg.push_back(b);
       }
     }
   }
-  sort_by_cost(v, qtile_cost);
+  sort_segment_major(v, seg, qtile_cost, conc_qtiles(s));
   return v;
 }
 
@@ -260,9 +305,10 @@ std::vector<char> replay_split_groups(const Shape& s, int mode) {
   return v;
 }
 
-// causal key tiles over contiguous segments [start, start+len)
-void causal_kvtiles(std::vector<KVTile>& v, int32_t start, int32_t len, int bn) {
+// causal key tiles over contiguous segments [start, start+len), segment id `id`
+void causal_kvtiles(std::vector<KVTile>& v, std::vector<int>& seg, int id, int32_t start, int32_t len, int bn) {
   for (int k0 = 0; k0 < len; k0 += bn) {
+    seg.push_back(id);
     KVTile t{};
     t.kv_row0 = start + k0;
     t.kv_len = std::min(bn, len - k0);
@@ -277,21 +323,24 @@ void causal_kvtiles(std::vector<KVTile>& v, int32_t start, int32_t len, int bn) 
 
 std::vector<KVTile> prefill_kvtiles(const Shape& s, int bn) {
   std::vector<KVTile> v;
-  for (int g = 0; g < s.ng; ++g) causal_kvtiles(v, s.cp[g], s.cp[g + 1] - s.cp[g], bn);
-  sort_by_cost(v, kvtile_cost);
+  std::vector<int> seg;
+  for (int g = 0; g < s.ng; ++g) causal_kvtiles(v, seg, g, s.cp[g], s.cp[g + 1] - s.cp[g], bn);
+  sort_segment_major(v, seg, kvtile_cost, conc_kvtiles(s));
   return v;
 }
 
 std::vector<KVTile> response_kvtiles(const Shape& s, int bn) {
   std::vector<KVTile> v;
-  for (int b = 0; b < s.nb; ++b) causal_kvtiles(v, s.cr[b], s.cr[b + 1] - s.cr[b], bn);
-  sort_by_cost(v, kvtile_cost);
+  std::vector<int> seg;
+  for (int b = 0; b < s.nb; ++b) causal_kvtiles(v, seg, b, s.cr[b], s.cr[b + 1] - s.cr[b], bn);
+  sort_segment_major(v, seg, kvtile_cost, conc_kvtiles(s));
   return v;
 }
 
 // prompt keys x every response row of the group, rows cut into n_seed chunks
 std::vector<KVTile> seed_kvtiles(const Shape& s, int bn, int n_seed, int bq) {
   std::vector<KVTile> v;
+  std::vector<int> seg;  // (group, chunk): the tiles of one segment sweep the same rows
   for (int g = 0; g < s.ng; ++g) {
     const int P = s.cp[g + 1] - s.cp[g];
     const int r0 = s.cr[s.cb[g]], r1 = s.cr[s.cb[g + 1]];
@@ -315,10 +364,11 @@ std::vector<KVTile> seed_kvtiles(const Shape& s, int bn, int n_seed, int bq) {
         t.causal = 0;
         t.part = c;
         v.push_back(t);
+        seg.push_back(g * n_seed + c);
       }
     }
   }
-  sort_by_cost(v, kvtile_cost);
+  sort_segment_major(v, seg, kvtile_cost, conc_kvtiles(s));
   return v;
 }
 
