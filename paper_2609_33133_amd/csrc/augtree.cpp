@@ -163,7 +163,10 @@ int64_t kvtile_cost(const KVTile& t) { return (int64_t)t.q_len * t.kv_len; }
 // start to the end of the launch has to cover `conc` (the tiles the chip runs
 // at once) times that tile. Segments that fail (the last, small ones; decided
 // from the end backwards) go to a pool at the end of the list, heaviest tile
-// first across the pooled segments.
+// first across the pooled segments. A launch shorter than a few rounds of its
+// heaviest tiles (less than 8 x conc x the heaviest tile in all) pools every
+// segment, i.e. keeps the plain heaviest-first order: there the tail of a
+// late heavy tile costs more than the shared reads save.
 template <class T, class F>
 void sort_segment_major(std::vector<T>& v, const std::vector<int>& seg, F cost, int conc) {
   int nseg = 0;
@@ -176,13 +179,19 @@ void sort_segment_major(std::vector<T>& v, const std::vector<int>& seg, F cost, 
   std::vector<int> order(nseg);
   std::iota(order.begin(), order.end(), 0);
   std::stable_sort(order.begin(), order.end(), [&](int a, int b) { return total[a] > total[b]; });
+  int64_t all = 0, top_all = 0;
+  for (int g = 0; g < nseg; ++g) {
+    all += total[g];
+    top_all = std::max(top_all, top[g]);
+  }
+  const bool shallow = all < 8 * (int64_t)conc * top_all;
   std::vector<int> rank(nseg, 0);
   std::vector<char> pooled(nseg, 0);
   int64_t after = 0;  // work listed after the segment being decided
   for (int k = nseg - 1; k >= 0; --k) {
     const int g = order[k];
     rank[g] = k;
-    if (after + total[g] < (int64_t)conc * top[g]) pooled[g] = 1;
+    if (shallow || after + total[g] < (int64_t)conc * top[g]) pooled[g] = 1;
     after += total[g];
   }
   std::vector<std::tuple<int, int, int64_t, size_t>> key(v.size());
