@@ -155,6 +155,60 @@ def test_determinism_bitwise():
                                outs[0][k].view(torch.uint8) if o[k].dtype != torch.float32 else outs[0][k]), k
 
 
+def _bits(t: torch.Tensor) -> torch.Tensor:
+    return t.contiguous().view(torch.uint8)
+
+
+def _batch_of(parts):
+    """Inputs of a batch made of single-tree inputs, in the given order."""
+    s0 = parts[0].shape
+    shape = I.custom_shape([p.shape.prompt_lens[0] for p in parts], [list(p.shape.branch_lens[0]) for p in parts],
+                           s0.num_q_heads, s0.num_kv_heads, s0.head_dim)
+    fields = {n: np.concatenate([getattr(p, n) for p in parts]) for n in
+              ("q_p", "k_p", "v_p", "q_r", "k_r", "v_r", "do_p", "do_r")}
+    return I.GroupInputs(shape=shape, **fields)
+
+
+def _run_step(gi, prefill_bwd_first=False):
+    b = GroupBatch.from_shape(gi.shape)
+    step = SharedStep(b, "cuda", mode=REPLAY_FUSED, n_seed=2)
+    x = upload(gi)
+    step.forward(x)
+    if prefill_bwd_first:
+        api.prefill_bwd(b, x["q_p"], x["k_p"], x["v_p"], step.o_p, step.lse_p, x["do_p"], step.dq_p, None,
+                        step.dkv_self, ws=step.ws["pb"])
+        api.replay_bwd(b, x["q_r"], x["k_r"], x["v_r"], x["k_p"], x["v_p"], step.o_r, step.lse_r, x["do_r"],
+                       step.n_seed, step.dq_r, step.dk_r, step.dv_r, step.seed, ws=step.ws["rb"])
+        api.prompt_grad_reduce(step.seed, self_part=step.dkv_self, out=step.dkv_p)
+    else:
+        step.backward(x)
+    torch.cuda.synchronize()
+    return {k: v.clone() for k, v in step.outputs().items()}
+
+
+def test_outputs_independent_of_batch_and_call_order():
+    """A tree's outputs are bitwise the same alone, first or second in a batch
+    (different tile schedules: the tiles of the other tree are interleaved or
+    ordered around them) and with the two backward calls in either order: every
+    output element is computed by one workgroup in a fixed order, and the
+    Eq. 2 sum runs in a fixed order (no atomics)."""
+    a = I.make_inputs(I.custom_shape([300], [[100, 200, 5]], 8, 2, 128), seed=21, qk_mult=1.0)
+    b = I.make_inputs(I.custom_shape([90], [[65, 129]], 8, 2, 128), seed=22)
+    alone = _run_step(a)
+    swapped = _run_step(a, prefill_bwd_first=True)
+    for k in alone:
+        assert torch.equal(_bits(swapped[k]), _bits(alone[k])), f"call order: {k}"
+    tp_a, tr_a, tp_b, tr_b = 300, 305, 90, 194
+    for parts, p0, r0 in (([a, b], 0, 0), ([b, a], tp_b, tr_b)):
+        got = _run_step(_batch_of(parts))
+        rows = {"o_p": (p0, tp_a), "dq_p": (p0, tp_a), "dk_p": (p0, tp_a), "dv_p": (p0, tp_a),
+                "o_r": (r0, tr_a), "dq_r": (r0, tr_a), "dk_r": (r0, tr_a), "dv_r": (r0, tr_a)}
+        for k, (o, n) in rows.items():
+            assert torch.equal(_bits(got[k][o:o + n]), _bits(alone[k])), f"batch position {p0}: {k}"
+        assert torch.equal(_bits(got["lse_p"][:, p0:p0 + tp_a]), _bits(alone["lse_p"])), "lse_p"
+        assert torch.equal(_bits(got["lse_r"][:, r0:r0 + tr_a]), _bits(alone["lse_r"])), "lse_r"
+
+
 @pytest.mark.parametrize("n_seed", [1, 2, 5])
 def test_seed_chunks_give_same_prompt_gradient(n_seed):
     shape = I.custom_shape([200], [[150, 150, 40, 300]], 8, 2, 128)
