@@ -44,6 +44,9 @@ SHAPES = [
     ([200, 33], [[100, 37, 64], [5]], 28, 4, 128, None),   # 28 / 4 heads: g = 7
     ([130], [[70, 1, 129]], 28, 4, 128, 1.0),              # g = 7, sharp
     ([96], [[3 + (7 * i) % 20 for i in range(64)]], 8, 2, 64, None),  # G = 64 short branches
+    ([200], [[100, 50]], 16, 2, 128, None),                # g = 8
+    ([150, 70], [[64, 129], [200]], 8, 8, 128, 1.0),       # g = 1 at d = 128, sharp
+    ([1], [[1000]], 4, 1, 64, 1.0),                        # one-token prompt, long branch, d = 64
 ]
 
 
