@@ -392,7 +392,7 @@ def main():
         print(summarize_trace(args.summarize_trace))
         return
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) > 1:
-        print("bench.py measures one GPU: this build has no multi-GPU path (the hot path shards by whole "
+        print("bench.py measures one GPU: the library has no multi-GPU path (the hot path shards by whole "
               "groups or KV heads with no exchange inside the op); run with --gpus 1", file=sys.stderr)
         sys.exit(2)
 
