@@ -46,7 +46,10 @@
  *   augtree_last_error() gives a detail string (thread-local). No C++
  *   exception crosses the ABI. Asynchronous kernel faults surface at the
  *   caller's next synchronisation, as in HIP.
- * Determinism: every output is bitwise reproducible run to run (no atomics).
+ * Determinism: every output is bitwise reproducible run to run (no atomics),
+ *   and a tree's outputs do not depend on the other trees of the batch (each
+ *   output element is computed by one workgroup in a fixed order, whatever
+ *   order the tiles are scheduled in).
  * Thread safety: calls are reentrant; calls on different streams that share a
  *   workspace race.
  */
