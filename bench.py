@@ -56,19 +56,18 @@ WORKLOAD_TEXT = {
 # launch role -> compiled kernel (template instantiation) it runs
 ROLE_KERNEL = {
     "fwd_prefill": "attn_fwd_kernel<bf16 out>", "fwd_replay": "attn_fwd_kernel<bf16 out>",
-    "fwd_replay_prompt": "attn_fwd_kernel<fp32 out>", "fwd_replay_own": "attn_fwd_kernel<fp32 out>",
-    "dkv_seed": "attn_dkv_kernel<fp32 out>", "dkv_prefill": "attn_dkv_kernel<fp32 out>",
-    "dkv_resp": "attn_dkv_kernel<bf16 out>",
-    "dq_replay": "attn_dq_kernel", "dq_prefill": "attn_dq_kernel",
-    "dsum_replay": "bwd_dsum_kernel", "dsum_prefill": "bwd_dsum_kernel", "lse_merge": "lse_merge_kernel",
-    "grad_reduce": "grad_reduce_kernel",
+    "fwd_tree": "attn_fwd_kernel<bf16 out>", "fwd_replay_split": "attn_fwd_kernel<fp32 out>",
+    "dkv_prefill": "attn_dkv_kernel", "dkv_replay": "attn_dkv_kernel", "dkv_tree": "attn_dkv_kernel",
+    "dq_prefill": "attn_dq_kernel", "dq_replay": "attn_dq_kernel", "dq_tree": "attn_dq_kernel",
+    "lse_merge": "lse_merge_kernel", "grad_reduce": "grad_reduce_kernel",
 }
-# launch role -> step of the method (the prefill / replay time breakdown)
+# launch role -> step of the method (the prefill / replay time breakdown of the
+# six-call path; the two-call path's launches hold both)
 ROLE_STEP = {
-    "fwd_prefill": "prefill_fwd", "fwd_replay": "replay_fwd", "fwd_replay_prompt": "replay_fwd",
-    "fwd_replay_own": "replay_fwd", "lse_merge": "replay_fwd", "dsum_replay": "replay_bwd", "dkv_seed": "replay_bwd",
-    "dkv_resp": "replay_bwd", "dq_replay": "replay_bwd", "dsum_prefill": "prefill_bwd", "dkv_prefill": "prefill_bwd",
-    "dq_prefill": "prefill_bwd", "grad_reduce": "prompt_grad_reduce",
+    "fwd_prefill": "prefill_fwd", "fwd_replay": "replay_fwd", "fwd_replay_split": "replay_fwd",
+    "lse_merge": "replay_fwd", "dkv_replay": "replay_bwd", "dq_replay": "replay_bwd",
+    "dkv_prefill": "prefill_bwd", "dq_prefill": "prefill_bwd", "grad_reduce": "prompt_grad_reduce",
+    "fwd_tree": "tree_fwd", "dq_tree": "tree_bwd", "dkv_tree": "tree_bwd",
 }
 # flops per (valid pair, query head) each attention role performs
 ROLE_FLOPS_PER_PAIR_D = {"fwd": 4, "dkv": 8, "dq": 6}
@@ -88,20 +87,17 @@ def role_work(role: str, shape, n_seed: int, split=None):
                 rp_split += sum(r * P for r in rs)
                 rr_split += sum(r * (r + 1) // 2 for r in rs)
                 rows_split += sum(rs)
+    replay = vp["replay_prompt"] + vp["replay_resp"]
     pairs = {
-        "fwd_prefill": vp["prefill"],
-        "fwd_replay": vp["replay_prompt"] + vp["replay_resp"] - rp_split - rr_split,
-        "fwd_replay_prompt": rp_split, "fwd_replay_own": rr_split,
-        "dkv_seed": vp["replay_prompt"], "dkv_resp": vp["replay_resp"], "dkv_prefill": vp["prefill"],
-        "dq_replay": vp["replay_prompt"] + vp["replay_resp"], "dq_prefill": vp["prefill"],
+        "fwd_prefill": vp["prefill"], "fwd_replay": replay - rp_split - rr_split,
+        "fwd_tree": vp["prefill"] + replay - rp_split - rr_split, "fwd_replay_split": rp_split + rr_split,
+        "dkv_prefill": vp["prefill"], "dkv_replay": replay, "dkv_tree": vp["shared"],
+        "dq_prefill": vp["prefill"], "dq_replay": replay, "dq_tree": vp["shared"],
     }
     if role in pairs:
         per = ROLE_FLOPS_PER_PAIR_D[role.split("_")[0]]
         return "flop", float(per * d * hq * pairs[role])
-    tp, tr, hkv = shape.total_prompt, shape.total_resp, shape.num_kv_heads
-    if role in ("dsum_replay", "dsum_prefill"):
-        rows = tr if role == "dsum_replay" else tp
-        return "byte", float(rows * hq * (2 * d * 2 + 4))
+    tp, hkv = shape.total_prompt, shape.num_kv_heads
     if role == "grad_reduce":
         e = 2 * tp * hkv * d
         return "byte", float(e * 4 * (1 + n_seed) + e * 2)
@@ -144,7 +140,7 @@ def bench_kernel_name(rocprof_name: str):
     if not m:
         return None
     base, targs = m.group(1), (m.group(3) or "")
-    if base in ("attn_fwd_kernel", "attn_dkv_kernel"):
+    if base == "attn_fwd_kernel":
         return base + ("<fp32 out>" if "true" in targs else "<bf16 out>")
     return base
 
@@ -158,10 +154,43 @@ def _counter_rows(path: str, counter: str):
     return out
 
 
-def summarize_pmc(d: str, workload: str) -> str:
+def algorithmic_bytes(role: str, shape, flat_rows: int = 0):
+    """Minimum HBM bytes of one launch of an attention role: every input read
+    once and every output written once (the prompt KV counted once). For the
+    flattened baseline's roles (tag "flattened") the inputs are its private
+    copies, `flat_rows` rows in all."""
+    hq, hkv, d = shape.num_q_heads, shape.num_kv_heads, shape.head_dim
+    tp, tr = shape.total_prompt, shape.total_resp
+    qrow, kvrow = hq * d * 2, hkv * d * 2
+    if role.startswith("flattened:"):
+        role, tp, tr = role.split(":", 1)[1], flat_rows, 0
+    role = role.split(":", 1)[-1]
+    if role == "fwd_prefill":      # Q_P, K_P, V_P -> O_P, LSE_P
+        return tp * (qrow + 2 * kvrow), tp * (qrow + hq * 4)
+    if role == "fwd_replay":       # Q_R, K_P, V_P, K_R, V_R -> O_R, LSE_R
+        return tr * qrow + (tp + tr) * 2 * kvrow, tr * (qrow + hq * 4)
+    if role == "fwd_tree":
+        return (tp + tr) * (qrow + 2 * kvrow), (tp + tr) * (qrow + hq * 4)
+    if role in ("dq_prefill", "dq_replay", "dq_tree"):   # Q, dO, O, LSE, K, V -> dQ, D
+        rows = {"dq_prefill": tp, "dq_replay": tr, "dq_tree": tp + tr}[role]
+        kv = tp if role == "dq_prefill" else tp + tr
+        return rows * (3 * qrow + hq * 4) + kv * 2 * kvrow, rows * (qrow + hq * 4)
+    if role in ("dkv_prefill", "dkv_replay", "dkv_tree"):  # Q, dO, LSE, D, K, V -> dK, dV (fp32 slabs or bf16)
+        rows = {"dkv_prefill": tp, "dkv_replay": tr, "dkv_tree": tp + tr}[role]
+        kv = {"dkv_prefill": tp, "dkv_replay": tp + tr, "dkv_tree": tp + tr}[role]
+        out = {"dkv_prefill": tp * 2 * hkv * d * 4, "dkv_replay": tp * 2 * hkv * d * 4 + tr * 2 * kvrow,
+               "dkv_tree": (tp + tr) * 2 * kvrow}[role]
+        return rows * (2 * qrow + hq * 8) + kv * 2 * kvrow, out
+    return None
+
+
+def summarize_pmc(d: str, workload: str, roles_file: str = None) -> str:
     """Markdown summary (with a machine-readable line) of the FETCH_SIZE and
     WRITE_SIZE passes in d/{fetch,write} and of the 1 GiB copy calibration
-    passes in d/{cfetch,cwrite} (rocprofv3 -f csv, file run_counter_collection.csv)."""
+    passes in d/{cfetch,cwrite} (rocprofv3 -f csv, file run_counter_collection.csv).
+    With `roles_file` (the launch roles of the profiled run in launch order,
+    written by --profile-roles), the library's dispatches are attributed to
+    their roles as well: per-role bytes against the role's algorithmic bytes."""
     def rows(sub, counter):
         return _counter_rows(os.path.join(d, sub, "run_counter_collection.csv"), counter)
     copy_bytes = 1 << 30
@@ -169,29 +198,54 @@ def summarize_pmc(d: str, workload: str) -> str:
     cw = max(v for _, v in rows("cwrite", "WRITE_SIZE"))
     f_scale = copy_bytes / (cf * 1024.0)
     w_scale = copy_bytes / (cw * 1024.0)
-    per = {}
+    roles = None
+    if roles_file:
+        with open(roles_file) as f:
+            roles = json.load(f)
+    per, per_role = {}, {}
     for sub, counter, scale, key in (("fetch", "FETCH_SIZE", f_scale, "fetch"), ("write", "WRITE_SIZE", w_scale, "write")):
-        for name, v in rows(sub, counter):
+        lib_rows = [(name, v) for name, v in rows(sub, counter) if bench_kernel_name(name) is not None]
+        if roles is not None and len(lib_rows) != len(roles["launches"]):
+            raise ValueError(f"{sub}: {len(lib_rows)} library dispatches but {len(roles['launches'])} logged launches")
+        for i, (name, v) in enumerate(lib_rows):
             k = bench_kernel_name(name)
-            if k is None:
-                continue
             e = per.setdefault(k, {"fetch": [], "write": []})
             e[key].append(v * 1024.0 * scale)
-    kernels = {}
-    for k, e in per.items():
+            if roles is not None:
+                r = roles["launches"][i]
+                if ROLE_KERNEL[r.split(":", 1)[-1]] != k:
+                    raise ValueError(f"dispatch {i}: kernel {k} but logged role {r}")
+                per_role.setdefault(r, {"fetch": [], "write": []})[key].append(v * 1024.0 * scale)
+
+    def avg(e):
         n = len(e["fetch"])
         fb = sum(e["fetch"]) / max(n, 1)
         wb = sum(e["write"]) / max(len(e["write"]), 1)
-        kernels[k] = {"launches": n, "fetch_bytes_per_launch": round(fb), "write_bytes_per_launch": round(wb),
-                      "bytes_per_launch": round(fb + wb)}
+        return {"launches": n, "fetch_bytes_per_launch": round(fb), "write_bytes_per_launch": round(wb),
+                "bytes_per_launch": round(fb + wb)}
+    kernels = {k: avg(e) for k, e in per.items()}
+    roles_out = {r: avg(e) for r, e in per_role.items()}
     data = {"workload": workload, "source_hash": kernel_source_hash(),
             "calibration": {"copy_bytes": copy_bytes, "copy_fetch_kib": cf, "copy_write_kib": cw,
                             "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
             "kernels": kernels}
+    if roles is not None:
+        data["roles"] = roles_out
     lines = ["| kernel | launches | HBM read GB / launch | HBM write GB / launch |", "|---|---|---|---|"]
     for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
         lines.append(f"| {k} | {v['launches']} | {v['fetch_bytes_per_launch'] / 1e9:.3f} | "
                      f"{v['write_bytes_per_launch'] / 1e9:.3f} |")
+    if roles is not None:
+        from paper_2609_33133_amd import inputs as I
+        shape = I.config_shape(workload)
+        lines += ["", "Per launch role (tag: the step that launched it):", "",
+                  "| role | launches | HBM read GB / launch | algorithmic read GB | HBM write GB / launch | "
+                  "algorithmic write GB |", "|---|---|---|---|---|---|"]
+        for r, v in sorted(roles_out.items()):
+            alg = algorithmic_bytes(r, shape, roles.get("flattened_rows", 0))
+            ar, aw = ("-", "-") if alg is None else (f"{alg[0] / 1e9:.3f}", f"{alg[1] / 1e9:.3f}")
+            lines.append(f"| {r} | {v['launches']} | {v['fetch_bytes_per_launch'] / 1e9:.3f} | {ar} | "
+                         f"{v['write_bytes_per_launch'] / 1e9:.3f} | {aw} |")
     lines.append("")
     lines.append(f"Copy calibration: a 1 GiB device copy reads {cf:.1f} KiB of FETCH_SIZE and writes {cw:.1f} KiB of "
                  f"WRITE_SIZE per dispatch, so the factors are {f_scale:.4f} (read) and {w_scale:.4f} (write).")
@@ -330,34 +384,192 @@ def time_steps(fn, steps: int, warmup: int):
     return ev[0].elapsed_time(ev[steps]) / steps, wall / steps * 1e3, per
 
 
-def cpu_baseline(gi, shared_flops: float):
-    """The fp64 oracle on one (group 0, query head 0, branch 0) flattened unit
-    of the workload, scaled to the whole job by flattened pair count."""
-    from threadpoolctl import threadpool_info
+_ORACLE_UNITS = None
+
+
+def _oracle_unit(i):
+    """Worker: one flattened (group, query head, branch) unit of the oracle,
+    single-threaded BLAS; returns its wall seconds (input decoding included)."""
+    from threadpoolctl import threadpool_limits
 
     from oracle import attention as A
     from paper_2609_33133_amd import inputs as I
+    gi, spec = _ORACLE_UNITS[0], _ORACLE_UNITS[1][i]
+    _, g, h, br, p0, p1, r0, r1, G = spec
     s = gi.shape
     c = I.bf16_bits_to_f64
-    p0, p1 = int(s.cu_prompt[0]), int(s.cu_prompt[1])
-    r0, r1 = int(s.cu_resp[0]), int(s.cu_resp[1])
-    kh = 0
-    args = [c(gi.q_p[p0:p1, :1]), c(gi.k_p[p0:p1, kh:kh + 1]), c(gi.v_p[p0:p1, kh:kh + 1]),
-            c(gi.q_r[r0:r1, :1]), c(gi.k_r[r0:r1, kh:kh + 1]), c(gi.v_r[r0:r1, kh:kh + 1]),
-            c(gi.do_p[p0:p1, :1]), c(gi.do_r[r0:r1, :1])]
-    P, R = p1 - p0, r1 - r0
+    kh = h // (s.num_q_heads // s.num_kv_heads)
+    with threadpool_limits(1):
+        t0 = time.perf_counter()
+        unit = (c(gi.q_p[p0:p1, h]), c(gi.k_p[p0:p1, kh]), c(gi.v_p[p0:p1, kh]), c(gi.q_r[r0:r1, h]),
+                c(gi.k_r[r0:r1, kh]), c(gi.v_r[r0:r1, kh]), c(gi.do_p[p0:p1, h]), c(gi.do_r[r0:r1, h]),
+                1.0 / G, s.scale)
+        A._flat_unit(unit)
+        return time.perf_counter() - t0
+
+
+def cpu_baseline(gi, shared_flops: float, budget_s: float = 20.0, max_workers: int = 16):
+    """The fp64 oracle (unchanged) timed on the host: its flattened units
+    (group, query head, branch), largest first, on a process pool with one
+    single-threaded worker per core (at most `max_workers`: the CPU share of
+    one GPU). Units are started until `budget_s` has passed; the ones started
+    are waited for. The whole job's time is extrapolated from the measured
+    wall time by the flattened pairs of the measured units."""
+    import multiprocessing as mp
+
+    global _ORACLE_UNITS
+    s = gi.shape
+    specs = []
+    for g in range(s.num_groups):
+        p0, p1 = int(s.cu_prompt[g]), int(s.cu_prompt[g + 1])
+        G = int(s.cu_branch[g + 1] - s.cu_branch[g])
+        for h in range(s.num_q_heads):
+            for br in range(int(s.cu_branch[g]), int(s.cu_branch[g + 1])):
+                r0, r1 = int(s.cu_resp[br]), int(s.cu_resp[br + 1])
+                L = (p1 - p0) + (r1 - r0)
+                specs.append((L * (L + 1) // 2, g, h, br, p0, p1, r0, r1, G))
+    specs.sort(key=lambda u: -u[0])
+    total_pairs = sum(u[0] for u in specs)
+    affinity = len(os.sched_getaffinity(0))
+    workers = max(1, min(affinity, max_workers))
+    units = specs                     # decoded inside the workers (forked: the inputs are shared)
+    _ORACLE_UNITS = (gi, specs)
+    done_pairs, done, unit_s = 0, 0, []
     t0 = time.perf_counter()
-    A.flattened_fwd_bwd([0, P], [0, 1], [0, R], 1, 1, s.scale, *args)
-    dt = time.perf_counter() - t0
-    unit_pairs = (P + R) * (P + R + 1) / 2
-    job_pairs = s.valid_pairs()["flattened"] * s.num_q_heads
-    est_job_s = dt * job_pairs / unit_pairs
-    threads = max([i.get("num_threads", 1) for i in threadpool_info() if i.get("user_api") == "blas"] or [1])
-    return {"value": round(shared_flops / est_job_s / 1e12, 6), "unit": "TFLOP/s", "cores": int(threads),
+    with mp.get_context("fork").Pool(workers) as pool:
+        pending = []
+        nxt = 0
+        while nxt < len(units) and (nxt < workers or time.perf_counter() - t0 < budget_s):
+            # keep at most `workers` units in flight
+            while nxt < len(units) and len([x for x in pending if not x[1].ready()]) < workers and \
+                    (nxt < workers or time.perf_counter() - t0 < budget_s):
+                pending.append((nxt, pool.apply_async(_oracle_unit, (nxt,))))
+                nxt += 1
+            time.sleep(0.05)
+        for i, r in pending:
+            unit_s.append(r.get())
+            done_pairs += specs[i][0]
+            done += 1
+    wall = time.perf_counter() - t0
+    _ORACLE_UNITS = None
+    est_job_s = wall * total_pairs / done_pairs
+    return {"value": round(shared_flops / est_job_s / 1e12, 6), "unit": "TFLOP/s", "cores": workers,
             "kind": "oracle",
-            "sample": f"flattened fp64 oracle on group 0, query head 0, branch 0 ([P={P}; R={R}], "
-                      f"{unit_pairs:.0f} pairs) in {dt:.1f} s; job time extrapolated by flattened pairs x heads "
-                      f"({job_pairs / unit_pairs:.0f} units): {est_job_s:.0f} s"}
+            "sample": f"fp64 oracle (flattened per-branch units: group, query head, branch), largest first, on "
+                      f"{workers} single-threaded workers ({affinity} cores in the affinity mask): {done} of "
+                      f"{len(specs)} units measured in {wall:.1f} s wall (unit times {min(unit_s):.1f}-"
+                      f"{max(unit_s):.1f} s); job time extrapolated by flattened pairs x{total_pairs / done_pairs:.1f}"
+                      f": {est_job_s:.0f} s",
+            "measured_units": done, "total_units": len(specs), "measured_s": round(wall, 2),
+            "extrapolation_factor": round(total_pairs / done_pairs, 3), "est_job_s": round(est_job_s, 1)}
+
+
+def device_inputs(shape, seed: int, device):
+    """Seeded inputs drawn on the GPU (torch's Philox generator): the same
+    distributions as the host recipe (Q, K, V ~ N(0,1)/sqrt(d), dO ~ N(0,1),
+    rounded to bf16), used for the per-config rows so that the large
+    workloads need no host-side generation."""
+    import torch
+    g = torch.Generator(device=device)
+    g.manual_seed(seed)
+    d = shape.head_dim
+    inv = 1.0 / math.sqrt(d)
+    tp, tr, hq, hkv = shape.total_prompt, shape.total_resp, shape.num_q_heads, shape.num_kv_heads
+    x = {}
+    for name, rows, heads, scale in (("q_p", tp, hq, inv), ("k_p", tp, hkv, inv), ("v_p", tp, hkv, inv),
+                                     ("q_r", tr, hq, inv), ("k_r", tr, hkv, inv), ("v_r", tr, hkv, inv),
+                                     ("do_p", tp, hq, None), ("do_r", tr, hq, None)):
+        t = torch.randn((rows, heads, d), generator=g, device=device, dtype=torch.float32)
+        if scale is not None:
+            t.mul_(scale)
+        x[name] = t.to(torch.bfloat16)
+        del t
+    return x
+
+
+# per-config rows: (steps, warmup) of the shared and the flattened step
+PER_CONFIG_STEPS = {"tiny": (200, 20), "balanced": (10, 3), "prompt": (10, 3), "response": (5, 2), "ragged": (2, 1)}
+
+
+def measure_config(name: str, mode: int, path: str, steps=None, warmup=None, flattened=True):
+    """ms per step of the shared step and of the flattened baseline on a named
+    workload (device inputs), and the derived rates."""
+    import torch
+
+    from paper_2609_33133_amd import inputs as I
+    from paper_2609_33133_amd.api import GroupBatch
+    from paper_2609_33133_amd.group_attention import FlattenedStep, SharedStep
+    s = I.config_shape(name)
+    st, wu = PER_CONFIG_STEPS.get(name, (5, 2))
+    st, wu = steps or st, warmup or wu
+    b = GroupBatch.from_shape(s)
+    x = device_inputs(s, 1000 + I.CONFIG_SEEDS[name], "cuda:0")
+    step = SharedStep(b, "cuda:0", mode=mode, path=path)
+    ms, wall_ms, per = time_steps(lambda: step.run(x), st, wu)
+    del step
+    torch.cuda.empty_cache()
+    flat_ms = None
+    if flattened:
+        fstep = FlattenedStep(b, "cuda:0")
+        fstep.materialize(x)
+        flat_ms, _, _ = time_steps(fstep.run, st, wu)
+        del fstep
+    del x
+    torch.cuda.empty_cache()
+    vp = s.valid_pairs()
+    counted = 14.0 * s.head_dim * s.num_q_heads * vp["shared"]
+    tf = counted / (ms * 1e-3) / 1e12
+    return {"workload": WORKLOAD_TEXT[name], "steps": st, "warmup": wu, "ms_per_step": round(ms, 4),
+            "median_ms": round(float(np.median(per)), 4), "host_wall_ms_per_step": round(wall_ms, 4),
+            "TFLOP/s": round(tf, 2), "pct_peak": round(100 * tf / PEAK_BF16_TFLOPS, 2),
+            "flattened_ms_per_step": None if flat_ms is None else round(flat_ms, 4),
+            "speedup_vs_flattened": None if flat_ms is None else round(flat_ms / ms, 3),
+            "work_ratio": round(vp["flattened"] / vp["shared"], 3)}
+
+
+def device_peak():
+    """bf16 dense MFMA peak from the device properties: CUs x peak engine
+    clock x 4096 flop per clock per CU (CDNA4: 4 SIMDs x 1024 flop/clk)."""
+    import torch
+    pr = torch.cuda.get_device_properties(0)
+    clock_khz = None
+    try:
+        from paper_2609_33133_amd import _lib  # noqa: F401
+        import ctypes.util  # noqa: F401
+        hip = ctypes.CDLL("libamdhip64.so")
+        v = ctypes.c_int(0)
+        # hipDeviceAttributeClockRate = 5 (kHz)
+        if hip.hipDeviceGetAttribute(ctypes.byref(v), 5, 0) == 0:
+            clock_khz = v.value
+    except OSError:
+        pass
+    cus = pr.multi_processor_count
+    peak = None if clock_khz is None else cus * clock_khz * 1e3 * 4096 / 1e12
+    return {"compute_units": cus, "peak_clock_mhz": None if clock_khz is None else clock_khz / 1e3,
+            "bf16_dense_tflops_from_device": None if peak is None else round(peak, 1)}
+
+
+class RoleLog:
+    """Logs the role of every library launch (launch hook), tagged with the
+    step that made it, for attributing counter dispatches to roles."""
+
+    def __init__(self, lib):
+        from paper_2609_33133_amd._lib import LAUNCH_HOOK
+        self.lib = lib
+        self.tag = "shared"
+        self.launches = []
+        self._cb = LAUNCH_HOOK(self._hook)
+
+    def _hook(self, role, phase, stream, user):
+        if phase == 0:
+            self.launches.append(f"{self.tag}:{role.decode()}")
+
+    def __enter__(self):
+        self.lib.augtree_set_launch_hook(self._cb, None)
+        return self
+
+    def __exit__(self, *a):
+        self.lib.augtree_set_launch_hook(ctypes.cast(None, type(self._cb)), None)
 
 
 def main():
@@ -368,12 +580,21 @@ def main():
     ap.add_argument("--workload", default="prompt", choices=sorted(WORKLOAD_TEXT))
     ap.add_argument("--mode", default="fused", choices=("fused", "split", "auto"),
                     help="replay forward: fused, split, or per group by the library's cost rule")
-    ap.add_argument("--n-seed", type=int, default=None)
+    ap.add_argument("--path", default="tree", choices=("tree", "calls"),
+                    help="tree: augtree_tree_fwd + augtree_tree_bwd; calls: the six separate entry points")
+    ap.add_argument("--n-seed", type=int, default=None, help="prompt-key chunks of the six-call path")
     ap.add_argument("--no-flattened", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
+    ap.add_argument("--no-per-config", action="store_true")
+    ap.add_argument("--no-breakdown", action="store_true")
+    ap.add_argument("--cpu-budget", type=float, default=20.0, help="seconds of oracle units to start")
+    ap.add_argument("--profile-roles", default=None, metavar="FILE",
+                    help="only run W + K steps of the shared step and of the flattened baseline with the launch "
+                         "roles logged to FILE (JSON), for attributing rocprofv3 counter dispatches; then exit")
     ap.add_argument("--summarize-pmc", default=None, metavar="DIR",
                     help="print the HBM traffic summary of rocprofv3 counter passes in DIR/{fetch,write,cfetch,cwrite} "
                          "(no GPU needed) and exit")
+    ap.add_argument("--roles", default=None, metavar="FILE", help="with --summarize-pmc: the --profile-roles log")
     ap.add_argument("--summarize-counters", default=None, metavar="DIR",
                     help="print MFMA busy %% and achieved HBM GB/s per kernel from rocprofv3 counter passes in "
                          "DIR/{sq,fetch,write,cfetch,cwrite} (no GPU needed) and exit")
@@ -383,7 +604,7 @@ def main():
                     help="only run a 1 GiB device-to-device copy 3 times (HBM counter calibration) and exit")
     args = ap.parse_args()
     if args.summarize_pmc:
-        print(summarize_pmc(args.summarize_pmc, args.workload))
+        print(summarize_pmc(args.summarize_pmc, args.workload, args.roles))
         return
     if args.summarize_counters:
         print(summarize_counters(args.summarize_counters))
@@ -417,41 +638,64 @@ def main():
         torch.cuda.synchronize()
         print(json.dumps({"copy_bytes_read": src.numel() * 4, "copy_bytes_written": dst.numel() * 4}))
         return
+    mode = {"fused": REPLAY_FUSED, "split": REPLAY_SPLIT, "auto": REPLAY_AUTO}[args.mode]
     print(f"[bench] building inputs: {args.workload}", file=sys.stderr, flush=True)
     gi = I.make_config(args.workload)
     s = gi.shape
     b = GroupBatch.from_shape(s)
     x = upload(gi, "cuda:0")
-    mode = {"fused": REPLAY_FUSED, "split": REPLAY_SPLIT, "auto": REPLAY_AUTO}[args.mode]
-    step = SharedStep(b, "cuda:0", mode=mode, n_seed=args.n_seed)
+    step = SharedStep(b, "cuda:0", mode=mode, n_seed=args.n_seed, path=args.path)
+
+    if args.profile_roles:
+        with RoleLog(lib) as log:
+            for _ in range(args.warmup + args.steps):
+                step.run(x)
+            torch.cuda.synchronize()
+            del step
+            torch.cuda.empty_cache()
+            log.tag = "flattened"
+            fstep = FlattenedStep(b, "cuda:0")
+            fstep.materialize(x)
+            for _ in range(args.warmup + args.steps):
+                fstep.run()
+            torch.cuda.synchronize()
+        with open(args.profile_roles, "w") as f:
+            json.dump({"workload": args.workload, "path": args.path, "launches": log.launches,
+                       "flattened_rows": int(fstep.tf)}, f)
+        print(f"[bench] {len(log.launches)} launches logged to {args.profile_roles}", file=sys.stderr, flush=True)
+        return
+
     vp = s.valid_pairs()
     counted = 14.0 * s.head_dim * s.num_q_heads * vp["shared"]
 
-    print("[bench] shared path", file=sys.stderr, flush=True)
+    print(f"[bench] shared path ({args.path})", file=sys.stderr, flush=True)
     ms, wall_ms, per_step = time_steps(lambda: step.run(x), args.steps, args.warmup)
     tflops = counted / (ms * 1e-3) / 1e12
 
-    # per-kernel durations over the same number of steps
-    with KernelTimer(lib) as kt:
-        for _ in range(args.steps):
-            step.run(x)
-        torch.cuda.synchronize()
-    per_role = kt.summary()
     split = None
     if mode == REPLAY_SPLIT:
         split = [1] * s.num_groups
     elif mode == REPLAY_AUTO:
         split = [int(v) for v in api.replay_split_groups(b)]
-    kernels, breakdown = {}, {}
-    for role, times in per_role.items():
-        k = ROLE_KERNEL[role]
-        kind, work = role_work(role, s, step.n_seed, split)
-        e = kernels.setdefault(k, {"ms": 0.0, "launches": 0, "work": 0.0, "kind": kind})
-        e["ms"] += float(np.sum(times))
-        e["launches"] += len(times)
-        e["work"] += work * args.steps
-        st = ROLE_STEP[role]
-        breakdown[st] = breakdown.get(st, 0.0) + float(np.sum(times)) / args.steps
+
+    def kernel_pass(st, n_seed):
+        """Per-kernel HIP-event durations over args.steps steps of `st`."""
+        with KernelTimer(lib) as kt:
+            for _ in range(args.steps):
+                st.run(x)
+            torch.cuda.synchronize()
+        kernels, breakdown = {}, {}
+        for role, times in kt.summary().items():
+            k = ROLE_KERNEL[role]
+            kind, work = role_work(role, s, n_seed, split)
+            e = kernels.setdefault(k, {"ms": 0.0, "launches": 0, "work": 0.0, "kind": kind})
+            e["ms"] += float(np.sum(times))
+            e["launches"] += len(times)
+            e["work"] += work * args.steps
+            breakdown[ROLE_STEP[role]] = breakdown.get(ROLE_STEP[role], 0.0) + float(np.sum(times)) / args.steps
+        return kernels, breakdown
+
+    kernels, breakdown = kernel_pass(step, step.n_seed)
     dom_name, dom = max(kernels.items(), key=lambda kv: kv[1]["ms"])
     avg_ms = dom["ms"] / dom["launches"]
     per_launch = dom["work"] / dom["launches"]
@@ -466,6 +710,7 @@ def main():
     roof["kernel"] = dom_name
     roof["avg_launch_ms"] = round(avg_ms, 4)
     roof["launches_per_step"] = dom["launches"] // args.steps
+    roof["work_per_launch"] = per_launch
     # HBM bytes per launch measured by the FETCH_SIZE / WRITE_SIZE counter
     # passes (copy-calibrated) on these exact sources, else null
     roof["traffic"] = recorded_traffic(args.workload, dom_name)
@@ -474,34 +719,68 @@ def main():
                         ("TFLOP/s" if v["kind"] == "flop" else "GB/s"):
                             round(v["work"] / (v["ms"] * 1e-3) / (1e12 if v["kind"] == "flop" else 1e9), 2)}
                     for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["ms"])}
-
     n_seed = int(step.n_seed)
+    del step
+    torch.cuda.empty_cache()
+
+    # prefill / replay breakdown: the six-call path puts each step of the
+    # method in launches of its own
+    calls_ms = None
+    if not args.no_breakdown and args.path == "tree":
+        print("[bench] six-call path (breakdown)", file=sys.stderr, flush=True)
+        cstep = SharedStep(b, "cuda:0", mode=mode, n_seed=args.n_seed, path="calls")
+        calls_ms, _, _ = time_steps(lambda: cstep.run(x), args.steps, args.warmup)
+        _, breakdown_calls = kernel_pass(cstep, cstep.n_seed)
+        breakdown.update(breakdown_calls)
+        del cstep
+        torch.cuda.empty_cache()
+
     flat_ms = None
     if not args.no_flattened:
         print("[bench] flattened baseline", file=sys.stderr, flush=True)
-        del step
-        torch.cuda.empty_cache()
         fstep = FlattenedStep(b, "cuda:0")
         fstep.materialize(x)
         flat_ms, _, _ = time_steps(fstep.run, args.steps, args.warmup)
         del fstep
         torch.cuda.empty_cache()
+    del x
+    torch.cuda.empty_cache()
+
+    per_config = None
+    if not args.no_per_config:
+        per_config = {}
+        for name in I.CONFIG_NAMES:
+            if name == args.workload:
+                per_config[name] = {"workload": WORKLOAD_TEXT[name], "steps": args.steps, "warmup": args.warmup,
+                                    "ms_per_step": round(ms, 4), "TFLOP/s": round(tflops, 2),
+                                    "pct_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+                                    "flattened_ms_per_step": None if flat_ms is None else round(flat_ms, 4),
+                                    "speedup_vs_flattened": None if flat_ms is None else round(flat_ms / ms, 3),
+                                    "work_ratio": round(vp["flattened"] / vp["shared"], 3),
+                                    "inputs": "host PCG64 recipe (the headline run)"}
+                continue
+            print(f"[bench] per-config row: {name}", file=sys.stderr, flush=True)
+            per_config[name] = measure_config(name, mode, args.path, flattened=not args.no_flattened)
+            per_config[name]["inputs"] = "device Philox draws, same distributions"
 
     cpu = None
     if not args.no_cpu:
         print("[bench] cpu oracle sample", file=sys.stderr, flush=True)
-        cpu = cpu_baseline(gi, counted)
+        cpu = cpu_baseline(gi, counted, budget_s=args.cpu_budget)
 
     line = {
         "metric": METRIC, "value": round(tflops, 2), "unit": "TFLOP/s", "n_gpus": 1, "steps": args.steps,
         "warmup": args.warmup, "ms_per_step": round(ms, 4), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
-        "config": {"workload": WORKLOAD_TEXT[args.workload], "replay_mode": args.mode,
-                   "n_seed": n_seed,
+        "config": {"workload": WORKLOAD_TEXT[args.workload], "replay_mode": args.mode, "path": args.path,
+                   "n_seed": n_seed if args.path == "calls" else None,
                    "counted_tflop_per_step": round(counted / 1e12, 4), "flop_convention": "14*d*Hq*valid_pairs"},
         "pct_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
+        "peak": {"bf16_dense_tflops_used": PEAK_BF16_TFLOPS, "source": "MI355X published dense bf16 MFMA peak",
+                 **device_peak()},
         "speedup_vs_flattened": None if flat_ms is None else round(flat_ms / ms, 3),
         "flattened_ms_per_step": None if flat_ms is None else round(flat_ms, 4),
+        "six_call_ms_per_step": None if calls_ms is None else round(calls_ms, 4),
         "host_wall_ms_per_step": round(wall_ms, 4),
         "step_ms": {"median": round(float(np.median(per_step)), 4), "min": round(float(np.min(per_step)), 4),
                     "max": round(float(np.max(per_step)), 4)},
@@ -509,9 +788,10 @@ def main():
         "tflops_12d": round(tflops * 12.0 / 14.0, 2),
         "roofline": roof,
         "kernels": kernel_table,
-        # time per step of each step of the method (prefill vs replay), from the per-launch events
+        # time per step of each step of the method, from the per-launch events
         "breakdown_ms": {k: round(v, 4) for k, v in breakdown.items()},
         "replay_split_groups": None if split is None else int(sum(split)),
+        "per_config": per_config,
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

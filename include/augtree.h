@@ -18,7 +18,10 @@
  *                 gradient ("seed") accumulated on the prompt KV (Eq. 2);
  *   prefill_bwd   gradients of the prefill (the prompt's own contribution);
  *   prompt_grad_reduce  the Eq. 2 sum of the prefill contribution and the
- *                 seeds, in a fixed order, without atomics.
+ *                 seeds, in a fixed order, without atomics;
+ *   tree_fwd / tree_bwd  the same step in two calls with fewer launches (the
+ *                 prefill and replay tiles share launches, and the Eq. 2 sum
+ *                 is formed in registers).
  *
  * Conventions shared by every entry point
  * ---------------------------------------
@@ -38,9 +41,12 @@
  *   from prefill_fwd until prefill_bwd.
  * Outputs are overwritten, never accumulated into.
  * Workspace: `ws` must hold augtree_workspace_size(...) bytes (256-byte
- *   aligned). The library writes a tile schedule there with an asynchronous
- *   host-to-device copy on `stream` (the host staging happens before the call
- *   returns), plus per-row scratch for the backward.
+ *   aligned). A launch of more than a few dozen tiles reads its tile schedule
+ *   from the workspace, written there with an asynchronous host-to-device copy
+ *   on `stream` (the host staging happens before the call returns); smaller
+ *   schedules travel in the kernel arguments. The backward also keeps
+ *   D = rowsum(dO * O) of every row there (written by its dQ kernel, read by
+ *   its dK/dV kernel).
  * Errors: every call returns an augtree_status. Arguments are validated on
  *   the host before any work is enqueued; on error nothing is launched and
  *   augtree_last_error() gives a detail string (thread-local). No C++
@@ -83,7 +89,9 @@ typedef enum augtree_op {
   AUGTREE_OP_PREFILL_FWD = 0,
   AUGTREE_OP_REPLAY_FWD = 1, /* workspace arg: replay mode */
   AUGTREE_OP_PREFILL_BWD = 2,
-  AUGTREE_OP_REPLAY_BWD = 3  /* workspace arg: n_seed */
+  AUGTREE_OP_REPLAY_BWD = 3, /* workspace arg: n_seed */
+  AUGTREE_OP_TREE_FWD = 4,   /* workspace arg: replay mode */
+  AUGTREE_OP_TREE_BWD = 5    /* workspace arg ignored */
 } augtree_op;
 
 /*
@@ -109,8 +117,9 @@ typedef struct augtree_groups {
 } augtree_groups;
 
 /* Bytes of workspace an entry point needs for this batch. `arg` is the replay
- * mode for AUGTREE_OP_REPLAY_FWD, n_seed for AUGTREE_OP_REPLAY_BWD, ignored
- * otherwise. Returns 0 on invalid arguments (see augtree_last_error). */
+ * mode for AUGTREE_OP_REPLAY_FWD / AUGTREE_OP_TREE_FWD, n_seed for
+ * AUGTREE_OP_REPLAY_BWD, ignored otherwise. Returns 0 on invalid arguments
+ * (see augtree_last_error). */
 size_t augtree_workspace_size(const augtree_groups* grp, int op, int arg);
 
 /*
@@ -195,6 +204,10 @@ int augtree_lse_merge(int64_t rows, int32_t heads, int32_t head_dim, int32_t n_p
  * In:  q_r, k_r, v_r, k_p, v_p, o_r (bf16), lse_r (fp32), do_r (bf16).
  * Out: dq_r [T_R,Hq,d], dk_r, dv_r [T_R,Hkv,d] bf16; dkv_p_seed fp32.
  * 1 <= n_seed <= 64.
+ * dQ: with dS rounded to bf16 for the dQ product, the kernel subtracts c times
+ * the row sum of the rounded dS, c = the group's first prompt key (exact in
+ * arithmetic since every row of dS sums to zero over its keys); this keeps a
+ * component shared by all keys from amplifying the rounding of dS.
  */
 int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uint16_t* k_r,
                        const uint16_t* v_r, const uint16_t* k_p, const uint16_t* v_p,
@@ -203,8 +216,9 @@ int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uin
                        size_t ws_bytes, void* stream);
 
 /*
- * Prompt prefill backward: the prompt queries' own contribution, computed
- * "through the original prompt-prefill graph" (§3.2), causal over P.
+ * Prompt prefill backward: the prompt queries' own contribution to every
+ * gradient, i.e. the backward of the causal prefill attention itself (§3.2;
+ * Eq. 2's first term for the prompt keys), causal over P.
  * In:  q_p, k_p, v_p, o_p (bf16), lse_p (fp32), do_p (bf16).
  * Out: dq_p [T_P,Hq,d] bf16 (nullable) and/or dq_p_f32 same shape fp32
  *      (nullable; at least one), dkv_p_self [2][T_P,Hkv,d] fp32 (0 = dK, 1 = dV).
@@ -214,6 +228,56 @@ int augtree_prefill_bwd(const augtree_groups* grp, const uint16_t* q_p, const ui
                         const uint16_t* v_p, const uint16_t* o_p, const float* lse_p,
                         const uint16_t* do_p, uint16_t* dq_p, float* dq_p_f32, float* dkv_p_self,
                         void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One tree step's forward in one call (§3.2: prefill once, then replay every
+ * branch against the stationary prompt KV; Eq. 1; §3.3). Computes exactly what
+ * augtree_prefill_fwd followed by augtree_replay_fwd compute (bit for bit:
+ * the same kernels and per-row arithmetic), but the prefill tiles and the
+ * fused replay tiles run in ONE kernel launch (fewer launches and one launch
+ * tail; the replay tiles read the prompt KV the prefill reads).
+ * mode: as for augtree_replay_fwd (SPLIT / AUTO groups add the fp32 partial
+ *   launch and the merge; o_part / lse_part are then required).
+ * In:  q_p [T_P,Hq,d], k_p, v_p [T_P,Hkv,d], q_r [T_R,Hq,d], k_r, v_r [T_R,Hkv,d] bf16.
+ * Out: o_p [T_P,Hq,d] bf16, lse_p [Hq,T_P], o_r [T_R,Hq,d] bf16, lse_r [Hq,T_R] fp32.
+ * Workspace: augtree_workspace_size(grp, AUGTREE_OP_TREE_FWD, mode).
+ */
+int augtree_tree_fwd(const augtree_groups* grp, int mode, const uint16_t* q_p, const uint16_t* k_p,
+                     const uint16_t* v_p, const uint16_t* q_r, const uint16_t* k_r, const uint16_t* v_r,
+                     uint16_t* o_p, float* lse_p, uint16_t* o_r, float* lse_r, float* o_part,
+                     float* lse_part, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * One tree step's backward in one call (§3.2 exact many-to-one backward;
+ * Eq. 2). The same gradients as augtree_replay_bwd + augtree_prefill_bwd +
+ * augtree_prompt_grad_reduce, in two kernel launches:
+ *   dQ launch: every prompt row (causal over the prompt) and every response
+ *     row (prompt keys, then its own causal keys); also forms
+ *     D = rowsum(dO * O) of every row into the workspace;
+ *   dK/dV launch: each prompt-key tile sweeps every response row of its group
+ *     (all branches, every prompt key visible) and then the prompt rows at or
+ *     after its first key (causal), so the whole Eq. 2 sum (branch seeds and
+ *     the prompt queries' own contribution) is accumulated in registers, in
+ *     that fixed order, and rounded once; each branch-key tile sweeps its
+ *     branch's rows (causal).
+ * The prompt gradient is the same sum as the three-call path up to fp32
+ * rounding order (that path adds two fp32 partial sums); it is bitwise
+ * reproducible. dQ carries the same common-mode correction as
+ * augtree_replay_bwd.
+ * In:  q_p, k_p, v_p, o_p (bf16), lse_p (fp32), do_p (bf16) [prompt rows];
+ *      q_r, k_r, v_r, o_r (bf16), lse_r (fp32), do_r (bf16) [response rows].
+ * Out: dq_p [T_P,Hq,d], dk_p, dv_p [T_P,Hkv,d], dq_r [T_R,Hq,d], dk_r, dv_r
+ *      [T_R,Hkv,d] bf16; dkv_p_f32 [2][T_P,Hkv,d] fp32 (nullable: the prompt
+ *      gradient before its bf16 rounding, 0 = dK, 1 = dV).
+ * Workspace: augtree_workspace_size(grp, AUGTREE_OP_TREE_BWD, 0).
+ */
+int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p,
+                     const uint16_t* v_p, const uint16_t* o_p, const float* lse_p,
+                     const uint16_t* do_p, const uint16_t* q_r, const uint16_t* k_r,
+                     const uint16_t* v_r, const uint16_t* o_r, const float* lse_r,
+                     const uint16_t* do_r, uint16_t* dq_p, uint16_t* dk_p, uint16_t* dv_p,
+                     float* dkv_p_f32, uint16_t* dq_r, uint16_t* dk_r, uint16_t* dv_r, void* ws,
+                     size_t ws_bytes, void* stream);
 
 /*
  * Eq. 2 reduction: the prompt-KV gradient is the prefill's own contribution
@@ -246,9 +310,9 @@ int augtree_prompt_grad_reduce(int32_t n_tensors, int64_t rows, int32_t heads, i
  * Launch hook (instrumentation; not part of the method). When set, `hook` is
  * called on the calling thread immediately before (phase 0) and after
  * (phase 1) every kernel launch the library enqueues from that thread, with a
- * static role name ("fwd_prefill", "fwd_replay", "fwd_replay_prompt",
- * "fwd_replay_own", "lse_merge", "dsum_replay", "dsum_prefill", "dkv_seed", "dkv_resp",
- * "dkv_prefill", "dq_replay", "dq_prefill", "grad_reduce") and the stream the
+ * static role name ("fwd_prefill", "fwd_replay", "fwd_tree", "fwd_replay_split",
+ * "lse_merge", "dq_prefill", "dkv_prefill", "dq_replay", "dkv_replay", "dq_tree",
+ * "dkv_tree", "grad_reduce") and the stream the
  * kernel is enqueued on, so that a caller can record HIP events around single
  * kernels. The hook must not call back into the library. NULL removes it.
  * Per thread; the library keeps no other state.

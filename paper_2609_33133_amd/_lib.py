@@ -29,12 +29,14 @@ OP_PREFILL_FWD = 0
 OP_REPLAY_FWD = 1
 OP_PREFILL_BWD = 2
 OP_REPLAY_BWD = 3
+OP_TREE_FWD = 4
+OP_TREE_BWD = 5
 
 EXPORTS = (
     "augtree_workspace_size", "augtree_prefill_fwd", "augtree_replay_fwd", "augtree_lse_merge",
     "augtree_replay_bwd", "augtree_prefill_bwd", "augtree_prompt_grad_reduce", "augtree_status_string",
     "augtree_last_error", "augtree_check_device", "augtree_version", "augtree_set_launch_hook",
-    "augtree_replay_split_groups",
+    "augtree_replay_split_groups", "augtree_tree_fwd", "augtree_tree_bwd",
 )
 
 LAUNCH_HOOK = ctypes.CFUNCTYPE(None, ctypes.c_char_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p)
@@ -85,6 +87,8 @@ def _sig(lib):
         "augtree_version": (ctypes.c_char_p, []),
         "augtree_set_launch_hook": (None, [LAUNCH_HOOK, ctypes.c_void_p]),
         "augtree_replay_split_groups": (ctypes.c_int, [_GP, _P]),
+        "augtree_tree_fwd": (ctypes.c_int, [_GP, ctypes.c_int] + [_P] * 12 + [_P, _SZ, _P]),
+        "augtree_tree_bwd": (ctypes.c_int, [_GP] + [_P] * 19 + [_P, _SZ, _P]),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)

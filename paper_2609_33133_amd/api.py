@@ -16,7 +16,8 @@ import numpy as np
 import torch
 
 from . import _lib
-from ._lib import REPLAY_FUSED, REPLAY_SPLIT, REPLAY_AUTO, OP_PREFILL_FWD, OP_REPLAY_FWD, OP_PREFILL_BWD, OP_REPLAY_BWD  # noqa: F401
+from ._lib import (REPLAY_FUSED, REPLAY_SPLIT, REPLAY_AUTO, OP_PREFILL_FWD, OP_REPLAY_FWD,  # noqa: F401
+                   OP_PREFILL_BWD, OP_REPLAY_BWD, OP_TREE_FWD, OP_TREE_BWD)
 
 
 def _ptr(t: Optional[torch.Tensor]):
@@ -220,3 +221,64 @@ def prompt_grad_reduce(parts, self_part=None, row_map=None, rows: Optional[int] 
                                                       part_stride, _ptr(parts), _ptr(row_map), _ptr(out),
                                                       _ptr(out_f32), _stream(stream)), "prompt_grad_reduce")
     return out, out_f32
+
+
+def tree_fwd(b: GroupBatch, q_p, k_p, v_p, q_r, k_r, v_r, mode: int = REPLAY_FUSED, o_p=None, lse_p=None, o_r=None,
+             lse_r=None, o_part=None, lse_part=None, ws=None, stream=None):
+    """Prefill + replay forward of every tree in one call (augtree_tree_fwd).
+    Returns (o_p, lse_p, o_r, lse_r, o_part, lse_part)."""
+    for t, nm, rows, h in ((q_p, "q_p", b.tp, b.hq), (k_p, "k_p", b.tp, b.hkv), (v_p, "v_p", b.tp, b.hkv),
+                           (q_r, "q_r", b.tr, b.hq), (k_r, "k_r", b.tr, b.hkv), (v_r, "v_r", b.tr, b.hkv)):
+        _need(t, nm, torch.bfloat16, (rows, h, b.d))
+    dev = q_p.device
+    o_p = torch.empty_like(q_p) if o_p is None else o_p
+    o_r = torch.empty_like(q_r) if o_r is None else o_r
+    lse_p = torch.empty((b.hq, b.tp), dtype=torch.float32, device=dev) if lse_p is None else lse_p
+    lse_r = torch.empty((b.hq, b.tr), dtype=torch.float32, device=dev) if lse_r is None else lse_r
+    _need(o_p, "o_p", torch.bfloat16, q_p.shape)
+    _need(o_r, "o_r", torch.bfloat16, q_r.shape)
+    _need(lse_p, "lse_p", torch.float32, (b.hq, b.tp))
+    _need(lse_r, "lse_r", torch.float32, (b.hq, b.tr))
+    if mode != REPLAY_FUSED:
+        o_part = torch.empty((2, b.tr, b.hq, b.d), dtype=torch.float32, device=dev) if o_part is None else o_part
+        lse_part = torch.empty((2, b.hq, b.tr), dtype=torch.float32, device=dev) if lse_part is None else lse_part
+    ws, nws = _ws(b, ws, OP_TREE_FWD, mode, dev)
+    _lib.check(_lib.load().augtree_tree_fwd(b.ref, mode, _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(q_r), _ptr(k_r),
+                                            _ptr(v_r), _ptr(o_p), _ptr(lse_p), _ptr(o_r), _ptr(lse_r), _ptr(o_part),
+                                            _ptr(lse_part), _ptr(ws), nws, _stream(stream)), "tree_fwd")
+    return o_p, lse_p, o_r, lse_r, o_part, lse_part
+
+
+def tree_bwd(b: GroupBatch, q_p, k_p, v_p, o_p, lse_p, do_p, q_r, k_r, v_r, o_r, lse_r, do_r, dq_p=None, dk_p=None,
+             dv_p=None, dkv_p_f32=None, dq_r=None, dk_r=None, dv_r=None, want_f32=False, ws=None, stream=None):
+    """Gradients of every tree in one call (augtree_tree_bwd): the Eq. 2 sum of
+    the prompt-key gradient is formed in registers. Returns
+    (dq_p, dk_p, dv_p, dq_r, dk_r, dv_r, dkv_p_f32 or None)."""
+    for t, nm, rows, h in ((q_p, "q_p", b.tp, b.hq), (k_p, "k_p", b.tp, b.hkv), (v_p, "v_p", b.tp, b.hkv),
+                           (o_p, "o_p", b.tp, b.hq), (do_p, "do_p", b.tp, b.hq),
+                           (q_r, "q_r", b.tr, b.hq), (k_r, "k_r", b.tr, b.hkv), (v_r, "v_r", b.tr, b.hkv),
+                           (o_r, "o_r", b.tr, b.hq), (do_r, "do_r", b.tr, b.hq)):
+        _need(t, nm, torch.bfloat16, (rows, h, b.d))
+    _need(lse_p, "lse_p", torch.float32, (b.hq, b.tp))
+    _need(lse_r, "lse_r", torch.float32, (b.hq, b.tr))
+    dev = q_p.device
+    dq_p = torch.empty_like(q_p) if dq_p is None else dq_p
+    dk_p = torch.empty_like(k_p) if dk_p is None else dk_p
+    dv_p = torch.empty_like(v_p) if dv_p is None else dv_p
+    dq_r = torch.empty_like(q_r) if dq_r is None else dq_r
+    dk_r = torch.empty_like(k_r) if dk_r is None else dk_r
+    dv_r = torch.empty_like(v_r) if dv_r is None else dv_r
+    for t, nm, ref in ((dq_p, "dq_p", q_p), (dk_p, "dk_p", k_p), (dv_p, "dv_p", v_p), (dq_r, "dq_r", q_r),
+                       (dk_r, "dk_r", k_r), (dv_r, "dv_r", v_r)):
+        _need(t, nm, torch.bfloat16, ref.shape)
+    if dkv_p_f32 is None and want_f32:
+        dkv_p_f32 = torch.empty((2, b.tp, b.hkv, b.d), dtype=torch.float32, device=dev)
+    if dkv_p_f32 is not None:
+        _need(dkv_p_f32, "dkv_p_f32", torch.float32, (2, b.tp, b.hkv, b.d))
+    ws, nws = _ws(b, ws, OP_TREE_BWD, 0, dev)
+    _lib.check(_lib.load().augtree_tree_bwd(b.ref, _ptr(q_p), _ptr(k_p), _ptr(v_p), _ptr(o_p), _ptr(lse_p),
+                                            _ptr(do_p), _ptr(q_r), _ptr(k_r), _ptr(v_r), _ptr(o_r), _ptr(lse_r),
+                                            _ptr(do_r), _ptr(dq_p), _ptr(dk_p), _ptr(dv_p), _ptr(dkv_p_f32),
+                                            _ptr(dq_r), _ptr(dk_r), _ptr(dv_r), _ptr(ws), nws, _stream(stream)),
+               "tree_bwd")
+    return dq_p, dk_p, dv_p, dq_r, dk_r, dv_r, dkv_p_f32

@@ -4,23 +4,22 @@
 
 Inputs are the packed bf16 tensors of a batch of replay trees (prompt rows
 [T_P, H, d], response rows [T_R, H, d], `batch` the GroupBatch holding their
-offsets). Forward: prefill_fwd (the prompt, causal, once per tree, §3.2) and
-replay_fwd (every branch against the stationary prompt KV plus its own causal
-KV, Eq. 1). Backward: replay_bwd (branch gradients and the prompt-KV gradient
-seeds of every branch, Eq. 2), prefill_bwd (the prompt queries' own
-contribution, through the prefill graph, §3.2) and prompt_grad_reduce (self
-plus seeds in a fixed order). Every step runs in the library's kernels on the
-current stream; autograd only routes tensors. There is no CPU path.
+offsets). Forward: augtree_tree_fwd (the prompt, causal, once per tree, and
+every branch against the stationary prompt KV plus its own causal KV; §3.2,
+Eq. 1). Backward: augtree_tree_bwd (branch gradients, and the prompt-KV
+gradient of every branch plus the prompt queries' own contribution summed on
+the prompt KV in a fixed order, Eq. 2). Every step runs in the library's
+kernels on the current stream; autograd only routes tensors. There is no CPU
+path.
 """
 from __future__ import annotations
 
-from typing import Optional, Tuple
+from typing import Tuple
 
 import torch
 
 from . import api
 from .api import REPLAY_FUSED, GroupBatch
-from .group_attention import default_n_seed
 
 
 def _check(t: torch.Tensor, name: str, rows: int, heads: int, d: int):
@@ -34,16 +33,15 @@ def _check(t: torch.Tensor, name: str, rows: int, heads: int, d: int):
 
 class _GroupAttention(torch.autograd.Function):
     @staticmethod
-    def forward(ctx, q_p, k_p, v_p, q_r, k_r, v_r, batch: GroupBatch, mode: int, n_seed: int):
+    def forward(ctx, q_p, k_p, v_p, q_r, k_r, v_r, batch: GroupBatch, mode: int):
         b = batch
         for t, n, rows, h in ((q_p, "q_p", b.tp, b.hq), (k_p, "k_p", b.tp, b.hkv), (v_p, "v_p", b.tp, b.hkv),
                               (q_r, "q_r", b.tr, b.hq), (k_r, "k_r", b.tr, b.hkv), (v_r, "v_r", b.tr, b.hkv)):
             _check(t, n, rows, h, b.d)
         q_p, k_p, v_p, q_r, k_r, v_r = (t.contiguous() for t in (q_p, k_p, v_p, q_r, k_r, v_r))
-        o_p, lse_p = api.prefill_fwd(b, q_p, k_p, v_p)
-        o_r, lse_r = api.replay_fwd(b, q_r, k_r, v_r, k_p, v_p, mode)[:2]
+        o_p, lse_p, o_r, lse_r = api.tree_fwd(b, q_p, k_p, v_p, q_r, k_r, v_r, mode)[:4]
         ctx.save_for_backward(q_p, k_p, v_p, q_r, k_r, v_r, o_p, lse_p, o_r, lse_r)
-        ctx.batch, ctx.n_seed = b, n_seed
+        ctx.batch = b
         ctx.mark_non_differentiable(lse_p, lse_r)
         return o_p, o_r
 
@@ -54,15 +52,13 @@ class _GroupAttention(torch.autograd.Function):
         # an output that did not reach the loss has a zero gradient
         do_p = torch.zeros_like(o_p) if do_p is None else do_p.to(torch.bfloat16).contiguous()
         do_r = torch.zeros_like(o_r) if do_r is None else do_r.to(torch.bfloat16).contiguous()
-        dq_r, dk_r, dv_r, seed = api.replay_bwd(b, q_r, k_r, v_r, k_p, v_p, o_r, lse_r, do_r, ctx.n_seed)
-        dq_p, _, dkv_self = api.prefill_bwd(b, q_p, k_p, v_p, o_p, lse_p, do_p)
-        dkv_p = api.prompt_grad_reduce(seed, self_part=dkv_self)[0]
-        return dq_p, dkv_p[0], dkv_p[1], dq_r, dk_r, dv_r, None, None, None
+        dq_p, dk_p, dv_p, dq_r, dk_r, dv_r, _ = api.tree_bwd(b, q_p, k_p, v_p, o_p, lse_p, do_p, q_r, k_r, v_r, o_r,
+                                                             lse_r, do_r)
+        return dq_p, dk_p, dv_p, dq_r, dk_r, dv_r, None, None
 
 
 def group_attention(q_p: torch.Tensor, k_p: torch.Tensor, v_p: torch.Tensor, q_r: torch.Tensor,
-                    k_r: torch.Tensor, v_r: torch.Tensor, batch: GroupBatch, mode: int = REPLAY_FUSED,
-                    n_seed: Optional[int] = None) -> Tuple[torch.Tensor, torch.Tensor]:
+                    k_r: torch.Tensor, v_r: torch.Tensor, batch: GroupBatch,
+                    mode: int = REPLAY_FUSED) -> Tuple[torch.Tensor, torch.Tensor]:
     """(O_P, O_R) of shared-prompt group attention; differentiable in all six inputs."""
-    return _GroupAttention.apply(q_p, k_p, v_p, q_r, k_r, v_r, batch, int(mode),
-                                 default_n_seed(batch) if n_seed is None else int(n_seed))
+    return _GroupAttention.apply(q_p, k_p, v_p, q_r, k_r, v_r, batch, int(mode))

@@ -41,26 +41,53 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
   const int tile_id = unit / p.hkv;
   const int kvh = unit - tile_id * p.hkv;
   const int head = kvh * p.group + hh;
-  const QTile t = p.tiles[tile_id];
+  const QTile t = load_tile(p.tiles, p.inl, tile_id);
+  const bool prow = (t.flags & QT_PROMPT_ROWS) != 0;  // prompt rows (prefill) or response rows
+  const uint16_t* const kb = prow ? p.kb[1] : p.kb[0];
+  const uint16_t* const vb = prow ? p.vb[1] : p.vb[0];
+  const int64_t lrows = prow ? p.lse_rows[1] : p.lse_rows[0];
   const int qi = wave * 32 + l32;
   const bool qvalid = qi < t.q_len;
   const int64_t qrow = (int64_t)t.q_row0 + qi;
   const int64_t qstride = (int64_t)p.hq * D;
   const int64_t kvstride = (int64_t)p.hkv * D;
 
+  // Q^T and dO^T operands: lane holds query qi, d = 16*ks + 8*hf .. +7.
+  // D = rowsum(dO * O) of the query is formed here from the same halves
+  // (eight partial sums, a tree, and the half-wave exchange) and stored for
+  // the dK/dV kernel.
   bf16x8 qreg[D / 16], doreg[D / 16];
+  float dsq;
   {
     const int64_t off = qrow * qstride + head * D + hf * 8;
+    const uint16_t* qs = (prow ? p.q[1] : p.q[0]) + off;
+    const uint16_t* ds = (prow ? p.dout[1] : p.dout[0]) + off;
+    const uint16_t* os = (prow ? p.o[1] : p.o[0]) + off;
+    float part[D / 16];
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks) {
-      qreg[ks] = as_bf16x8(qvalid ? ldg16(p.q + off + ks * 16) : make_uint4(0, 0, 0, 0));
-      doreg[ks] = as_bf16x8(qvalid ? ldg16(p.dout + off + ks * 16) : make_uint4(0, 0, 0, 0));
+      const uint4 z = make_uint4(0, 0, 0, 0);
+      qreg[ks] = as_bf16x8(qvalid ? ldg16(qs + ks * 16) : z);
+      const uint4 dv = qvalid ? ldg16(ds + ks * 16) : z;
+      const uint4 ov = qvalid ? ldg16(os + ks * 16) : z;
+      doreg[ks] = as_bf16x8(dv);
+      float a = 0.f;
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        a += __uint_as_float(half16(dv, e) << 16) * __uint_as_float(half16(ov, e) << 16);
+      part[ks] = a;
     }
+#pragma unroll
+    for (int w = D / 32; w >= 1; w >>= 1)
+#pragma unroll
+      for (int ks = 0; ks < w; ++ks) part[ks] += part[ks + w];
+    dsq = pair_sum(part[0]);
   }
+  if (qvalid && hf == 0) (prow ? p.dsum[1] : p.dsum[0])[(int64_t)head * lrows + qrow] = dsq;
   // S and dP accumulators start at -LSE / scale and -D of this lane's query,
   // so the MFMAs leave S - LSE / scale and dP - D: P = exp2(c * s), dS = P * dp
-  const float nlse = qvalid ? -p.lse[(int64_t)head * p.lse_rows + qrow] / p.scale : 0.f;
-  const float dsq = qvalid ? p.dsum[(int64_t)head * p.lse_rows + qrow] : 0.f;
+  const float nlse = qvalid ? -(prow ? p.lse[1] : p.lse[0])[(int64_t)head * lrows + qrow] / p.scale : 0.f;
+  if (!qvalid) dsq = 0.f;
   const float c = p.scale_log2;
 
   f32x16 acc[D / 32];
@@ -68,6 +95,9 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
   for (int db = 0; db < D / 32; ++db)
 #pragma unroll
     for (int i = 0; i < 16; ++i) acc[db][i] = 0.f;
+  // sum over the keys of dS as rounded to bf16 for the dQ MFMAs (this lane's
+  // 16 keys of every 32-key half); see the correction at the end
+  float ds_sum = 0.f;
 
   const int nA = (t.a_len + DQ_BN - 1) / DQ_BN;
   const int nB = (t.b_len + DQ_BN - 1) / DQ_BN;
@@ -81,8 +111,8 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
     const int len = isB ? t.b_len : t.a_len;
     const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
     const int nvalid = min(DQ_BN, len - kb0);
-    cp.issue(kd, isB ? p.kb : p.ka, row0, nvalid, kvstride, kvh * D);
-    cp.issue(vd, isB ? p.vb : p.va, row0, nvalid, kvstride, kvh * D);
+    cp.issue(kd, isB ? kb : p.ka, row0, nvalid, kvstride, kvh * D);
+    cp.issue(vd, isB ? vb : p.va, row0, nvalid, kvstride, kvh * D);
   };
 
   RowOffsets<D> r0_off, r1_off;  // K/V rows l32 and 32 + l32
@@ -125,6 +155,7 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 #pragma unroll
       for (int i = 0; i < 16; ++i) s[i] = __builtin_amdgcn_exp2f(s[i] * c) * dp[i];
       const bf16x8 g0 = to_bf16x8(s, 0), g1 = to_bf16x8(s, 8);
+      ds_sum = sum_bf16x8(g0, sum_bf16x8(g1, ds_sum));
       set_wave_priority<0>();
 #pragma unroll
       for (int db = 0; db < D / 32; ++db) {
@@ -139,6 +170,34 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
   if (nblk > 0) load_block(0, k_buf0, v_buf0);
   wait_vmem();
   __syncthreads();
+  // The vector c of the common-mode correction at the end: the mean of the
+  // group's first (up to) 64 prompt keys of KV head kvh. They are block 0 of
+  // every tile's sweep (segment A's first block for response rows, segment
+  // B's for prompt rows), now in k_buf0. Wave w sums rows 16w .. 16w + 15
+  // (lane l: 16-byte chunk l % CH of rows 16w + l / CH + k * 64 / CH), the
+  // lanes of one chunk are added, and the four waves' partial sums go to LDS.
+  __shared__ float kmean_part[4][D];
+  {
+    constexpr int CH = D / 8;
+    const int ch = lane % CH;
+    float part[8];
+#pragma unroll
+    for (int e = 0; e < 8; ++e) part[e] = 0.f;
+#pragma unroll
+    for (int k = 0; k < CH / 4; ++k) {
+      const int r = 16 * wave + lane / CH + k * (64 / CH);
+      const uint4 v = *reinterpret_cast<const uint4*>(k_buf0 + r * D + ((ch ^ swz<D>(r)) << 3));
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part[e] += __uint_as_float(half16(v, e) << 16);
+    }
+#pragma unroll
+    for (int off = CH; off < 64; off <<= 1)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) part[e] += __shfl_xor(part[e], off);
+    if (lane < CH)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) kmean_part[wave][ch * 8 + e] = part[e];
+  }
   for (int b = 0; b < nblk; b += 2) {
     if (b + 1 < nblk) load_block(b + 1, k_buf1, v_buf1);
     compute(b, k_buf0, v_buf0);
@@ -152,21 +211,39 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
     }
   }
 
+  // Common-mode correction. Every row of dS sums to zero over its keys
+  // (sum_j P_j dP_j = dO.O = D), so dQ = s sum_j dS_j (k_j - c) for any vector
+  // c. The MFMAs form sum_j dS~_j k_j with dS~ = dS rounded to bf16; when the
+  // keys share a large component, the rounding error of dS~ is multiplied by
+  // it while dQ itself only sees the keys' differences. Subtracting c times
+  // the sum of the same rounded values gives sum_j dS~_j (k_j - c) exactly
+  // (up to fp32 accumulation): with c the mean of the group's first keys, a
+  // component shared by the keys no longer multiplies the rounding error.
+  const float ds_tot = pair_sum(ds_sum);
+  const float inv_n0 = 1.f / (float)min(DQ_BN, t.a_len > 0 ? t.a_len : t.b_len);
   if (qvalid) {
     const int64_t obase = qrow * qstride + head * D;
+    uint16_t* const dq16 = prow ? p.dq[1] : p.dq[0];
+    float* const dq32 = prow ? p.dq32[1] : p.dq32[0];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
       for (int g4 = 0; g4 < 4; ++g4) {
         const int dd = db * 32 + g4 * 8 + hf * 4;
-        const float v0 = acc[db][g4 * 4 + 0] * p.scale, v1 = acc[db][g4 * 4 + 1] * p.scale;
-        const float v2 = acc[db][g4 * 4 + 2] * p.scale, v3 = acc[db][g4 * 4 + 3] * p.scale;
-        if (p.dq32) *reinterpret_cast<float4*>(p.dq32 + obase + dd) = make_float4(v0, v1, v2, v3);
-        if (p.dq) {
+        f32x4 cs = *reinterpret_cast<const f32x4*>(&kmean_part[0][dd]);
+#pragma unroll
+        for (int w = 1; w < 4; ++w) cs += *reinterpret_cast<const f32x4*>(&kmean_part[w][dd]);
+        const float corr = ds_tot * inv_n0;
+        const float v0 = (acc[db][g4 * 4 + 0] - corr * cs[0]) * p.scale;
+        const float v1 = (acc[db][g4 * 4 + 1] - corr * cs[1]) * p.scale;
+        const float v2 = (acc[db][g4 * 4 + 2] - corr * cs[2]) * p.scale;
+        const float v3 = (acc[db][g4 * 4 + 3] - corr * cs[3]) * p.scale;
+        if (dq32) *reinterpret_cast<float4*>(dq32 + obase + dd) = make_float4(v0, v1, v2, v3);
+        if (dq16) {
           typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
           bf16x4 w;
           w[0] = (__bf16)v0; w[1] = (__bf16)v1; w[2] = (__bf16)v2; w[3] = (__bf16)v3;
-          *reinterpret_cast<bf16x4*>(p.dq + obase + dd) = w;
+          *reinterpret_cast<bf16x4*>(dq16 + obase + dd) = w;
         }
       }
     }
@@ -180,7 +257,7 @@ constexpr int KV_BQ = 64;   // query rows per block (32 per wavefront of a pair)
 constexpr int DKV_SDP_DEPTH = 3;  // LDS operand reads of S / dP run this many MFMAs ahead
 constexpr int DKV_DVK_DEPTH = 2;  // the same for the dV / dK transpose reads
 
-template <int D, bool OUT32>
+template <int D>
 __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   // the workgroup's K and V tiles (operands of S = Q K^T and dP = dO V^T);
   // query blocks double-buffered in separate arrays, with -LSE / scale and
@@ -203,18 +280,19 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   const int qs = wave_u >> 2;  // 32-row half of every query block
   const int tile_id = blockIdx.x / p.hkv;
   const int kvh = blockIdx.x - tile_id * p.hkv;
-  const KVTile t = p.tiles[tile_id];
+  const KVTile t = load_tile(p.tiles, p.inl, tile_id);
+  const int pk = (t.flags & KV_PROMPT_KEYS) ? 1 : 0;  // prompt keys or branch keys
+  const bool x_causal = (t.flags & KV_X_CAUSAL) != 0;
   const int kw0 = kq * 32;
   const int kj = kw0 + l32;  // this lane's key (B-operand column)
-  const bool kvalid = kj < t.kv_len;
   const int64_t qstride = (int64_t)p.hq * D;
   const int64_t kvstride = (int64_t)p.hkv * D;
 
   {
     TileCopy<KV_BN, D, 8> kc;
     kc.init(kvstride);
-    kc.issue(k_tile, p.k, t.kv_row0, t.kv_len, kvstride, kvh * D);
-    kc.issue(v_tile, p.v, t.kv_row0, t.kv_len, kvstride, kvh * D);
+    kc.issue(k_tile, pk ? p.k[1] : p.k[0], t.kv_row0, t.kv_len, kvstride, kvh * D);
+    kc.issue(v_tile, pk ? p.v[1] : p.v[0], t.kv_row0, t.kv_len, kvstride, kvh * D);
   }
   f32x16 dk[D / 32], dv[D / 32];
 #pragma unroll
@@ -223,8 +301,30 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     for (int i = 0; i < 16; ++i) { dk[db][i] = 0.f; dv[db][i] = 0.f; }
 
   const float c = p.scale_log2;
-  const int nqb = (t.q_len + KV_BQ - 1) / KV_BQ;
-  const int nblk = p.group * nqb;
+  // query blocks: range X (response rows) then range Y (prompt rows)
+  const int nxb = (t.x_len + KV_BQ - 1) / KV_BQ;
+  const int nyb = (t.y_len + KV_BQ - 1) / KV_BQ;
+  const int nxblk = p.group * nxb;
+  const int nblk = nxblk + p.group * nyb;
+
+  // Block b -> (range, query head, 64-row block). Inside a range the query
+  // blocks are swept from the end backwards and the g heads of a block are
+  // taken one after the other, so that the concurrent tiles of one KV head
+  // (causal ranges all end at the segment end; the response rows of a group
+  // are the same for all its prompt key tiles) stay at the same query rows
+  // and share the Q / dO blocks in L2.
+  struct Blk {
+    int y, hh, qb;
+  };
+  auto block_of = [&](int b) -> Blk {
+    Blk r;
+    r.y = b >= nxblk;
+    const int bb = r.y ? b - nxblk : b;
+    const int nb = r.y ? nyb : nxb;
+    r.hh = kvh * p.group + bb % p.group;
+    r.qb = nb - 1 - bb / p.group;
+    return r;
+  };
 
   // Wavefront 0 loads the raw LSE and wavefront 1 the D values of the next
   // query block into `stat`; they are scaled and stored to LDS at the end of
@@ -234,20 +334,21 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   int stat_n = 0;
   TileCopy<KV_BQ, D, 8> qc;
   qc.init(qstride);
-  // Block b is query block nqb - 1 - b / group of query head b % group: the
-  // query blocks are swept from the end of the range backwards and the g
-  // heads of a block are taken one after the other, so that the concurrent
-  // tiles of one KV head (causal ranges all end at the segment end) stay at
-  // the same query rows and share the Q / dO blocks in L2.
+  // the query-side tensors of both ranges, read from the kernel arguments
+  // once (a per-block indexed read of the arguments would be a scalar load
+  // plus a wait in the loop)
+  const uint16_t* const q_src[2] = {p.q[0], p.q[1]};
+  const uint16_t* const do_src[2] = {p.dout[0], p.dout[1]};
+  const float* const st_src[2] = {wave_u == 0 ? p.lse[0] : p.dsum[0], wave_u == 0 ? p.lse[1] : p.dsum[1]};
+  const int64_t st_rows[2] = {p.lse_rows[0], p.lse_rows[1]};
   auto load_block = [&](int b, __bf16* qd, __bf16* od) {
-    const int hh = kvh * p.group + b % p.group;
-    const int qb = nqb - 1 - b / p.group;
-    const int64_t row0 = (int64_t)t.q_row0 + qb * KV_BQ;
-    const int nvalid = min(KV_BQ, t.q_len - qb * KV_BQ);
-    qc.issue(qd, p.q, row0, nvalid, qstride, hh * D);
-    qc.issue(od, p.dout, row0, nvalid, qstride, hh * D);
+    const Blk k = block_of(b);
+    const int64_t row0 = (int64_t)(k.y ? t.y_row0 : t.x_row0) + k.qb * KV_BQ;
+    const int nvalid = min(KV_BQ, (k.y ? t.y_len : t.x_len) - k.qb * KV_BQ);
+    qc.issue(qd, k.y ? q_src[1] : q_src[0], row0, nvalid, qstride, k.hh * D);
+    qc.issue(od, k.y ? do_src[1] : do_src[0], row0, nvalid, qstride, k.hh * D);
     if (wave_u < 2) {
-      const float* src = (wave_u == 0 ? p.lse : p.dsum) + (int64_t)hh * p.lse_rows + row0;
+      const float* src = (k.y ? st_src[1] : st_src[0]) + (int64_t)k.hh * (k.y ? st_rows[1] : st_rows[0]) + row0;
       stat = src[min(lane, nvalid - 1)];
       stat_n = nvalid;
     }
@@ -260,7 +361,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     else if (wave_u == 1) dd[lane] = lane < stat_n ? -stat : 0.f;
   };
 
-  const int key_pos = t.kpos0 + kj;  // this lane's key position (causal tiles)
+  const int key_pos = t.kpos0 + kj;  // this lane's key position (causal ranges)
   RowOffsets<D> qrow_off, key_off;   // Q/dO rows of this wave's half; K/V rows of its keys
   qrow_off.init(qs * 32 + l32, hf);
   key_off.init(kj, hf);
@@ -271,11 +372,12 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   TrOffsets<D> qtr_off;              // Q^T / dO^T operands of this wave's half
   qtr_off.init(qs * 32, lane);
   auto compute = [&](int b, const __bf16* ql, const __bf16* dl, const float* lsel, const float* dsl) {
-    const int qb = nqb - 1 - b / p.group;
-    const int qpos0 = t.qpos0 + qb * KV_BQ + qs * 32;  // position of this wave's first query
-    const bool skip = t.causal && (qpos0 + 31 < t.kpos0 + kw0);
+    const Blk k = block_of(b);
+    const bool causal = k.y || x_causal;
+    const int qpos0 = t.kpos0 + k.qb * KV_BQ + qs * 32;  // position of this wave's first query (causal)
+    const bool skip = causal && (qpos0 + 31 < t.kpos0 + kw0);
     if (skip) return;
-    const bool need_mask = t.causal && (qpos0 < t.kpos0 + kw0 + 31);
+    const bool need_mask = causal && (qpos0 < t.kpos0 + kw0 + 31);
     // S and dP accumulators start at -LSE / scale and -D of their rows
     // (register i holds row g4 * 8 + 4 * hf + e, i = 4 * g4 + e), so the
     // MFMAs leave S - LSE / scale and dP - D: P = exp2(c * s), dS = P * dp.
@@ -372,6 +474,10 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   if (qs != 0) return;
 
   // dK/dV tile: lane holds column d = 32*db + l32, rows = keys acc_row(i, hf)
+  uint16_t* const dk16 = (t.flags & KV_OUT_BF16) ? p.dk[pk] : nullptr;
+  uint16_t* const dv16 = (t.flags & KV_OUT_BF16) ? p.dv[pk] : nullptr;
+  const int64_t slab = p.slab_rows * kvstride;
+  float* const dk32 = (t.flags & KV_OUT_SLAB) ? p.slab + 2 * (int64_t)(t.flags >> KV_PART_SHIFT) * slab : nullptr;
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
@@ -381,45 +487,16 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
         const int64_t row = (int64_t)t.kv_row0 + key;
         const int64_t off = row * kvstride + kvh * D + db * 32 + l32;
         const float kval = dk[db][i] * p.scale, vval = dv[db][i];
-        if constexpr (OUT32) {
-          const int64_t slab = (int64_t)p.out_rows * kvstride;
-          p.dkv32[(2 * (int64_t)t.part) * slab + off] = kval;
-          p.dkv32[(2 * (int64_t)t.part + 1) * slab + off] = vval;
-        } else {
-          reinterpret_cast<__bf16*>(p.dk)[off] = (__bf16)kval;
-          reinterpret_cast<__bf16*>(p.dv)[off] = (__bf16)vval;
+        if (dk32) {
+          dk32[off] = kval;
+          dk32[slab + off] = vval;
+        }
+        if (dk16) {
+          reinterpret_cast<__bf16*>(dk16)[off] = (__bf16)kval;
+          reinterpret_cast<__bf16*>(dv16)[off] = (__bf16)vval;
         }
       }
     }
-  }
-}
-
-// ----------------------------------------------------------------------------- D = rowsum(dO * O)
-
-template <int D>
-__global__ __launch_bounds__(256) void bwd_dsum_kernel(const uint16_t* o, const uint16_t* dout, float* dsum,
-                                                       int64_t rows, int hq) {
-  constexpr int CH = D / 8;
-  const int64_t gid = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  const int64_t rh = gid / CH;
-  const int ch = (int)(gid % CH);
-  float acc = 0.f;
-  if (rh < rows * hq) {
-    const uint4 a = ldg16(o + rh * D + ch * 8);
-    const uint4 b = ldg16(dout + rh * D + ch * 8);
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const float x = __uint_as_float(half16(a, e) << 16);
-      const float y = __uint_as_float(half16(b, e) << 16);
-      acc += x * y;
-    }
-  }
-#pragma unroll
-  for (int off = CH / 2; off > 0; off >>= 1) acc += __shfl_xor(acc, off);
-  if (ch == 0 && rh < rows * hq) {
-    const int64_t row = rh / hq;
-    const int h = (int)(rh - row * hq);
-    dsum[(int64_t)h * rows + row] = acc;
   }
 }
 
@@ -435,26 +512,11 @@ hipError_t launch_attn_dq(const DqParams& p0, int n_tiles, hipStream_t stream) {
   return hipGetLastError();
 }
 
-hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, bool out_f32, hipStream_t stream) {
+hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, hipStream_t stream) {
   if (n_tiles == 0) return hipSuccess;
   const dim3 grid((unsigned)n_tiles * (unsigned)p.hkv), block(512);
-  if (p.head_dim == 128) {
-    if (out_f32) hipLaunchKernelGGL((attn_dkv_kernel<128, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((attn_dkv_kernel<128, false>), grid, block, 0, stream, p);
-  } else {
-    if (out_f32) hipLaunchKernelGGL((attn_dkv_kernel<64, true>), grid, block, 0, stream, p);
-    else hipLaunchKernelGGL((attn_dkv_kernel<64, false>), grid, block, 0, stream, p);
-  }
-  return hipGetLastError();
-}
-
-hipError_t launch_bwd_dsum(const uint16_t* o, const uint16_t* dout, float* dsum, int64_t rows, int hq,
-                           int head_dim, hipStream_t stream) {
-  const int64_t threads = rows * hq * (head_dim / 8);
-  if (threads == 0) return hipSuccess;
-  const dim3 grid((unsigned)((threads + 255) / 256)), block(256);
-  if (head_dim == 128) hipLaunchKernelGGL((bwd_dsum_kernel<128>), grid, block, 0, stream, o, dout, dsum, rows, hq);
-  else hipLaunchKernelGGL((bwd_dsum_kernel<64>), grid, block, 0, stream, o, dout, dsum, rows, hq);
+  if (p.head_dim == 128) hipLaunchKernelGGL((attn_dkv_kernel<128>), grid, block, 0, stream, p);
+  else hipLaunchKernelGGL((attn_dkv_kernel<64>), grid, block, 0, stream, p);
   return hipGetLastError();
 }
 

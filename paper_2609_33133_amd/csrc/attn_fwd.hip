@@ -50,7 +50,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   const int tile_id = unit / p.hkv;
   const int kvh = unit - tile_id * p.hkv;
   const int head = kvh * p.group + hh;
-  const QTile t = p.tiles[tile_id];
+  const QTile t = load_tile(p.tiles, p.inl, tile_id);
+  // prompt rows (prefill) or response rows (replay): tensors of the tile
+  const bool prow = (t.flags & QT_PROMPT_ROWS) != 0;
+  const uint16_t* const qsrc = prow ? p.q[1] : p.q[0];
+  const uint16_t* const kb = prow ? p.kb[1] : p.kb[0];
+  const uint16_t* const vb = prow ? p.vb[1] : p.vb[0];
   const int qi = wave * 32 + l32;
   const bool qvalid = qi < t.q_len;
   const int64_t qrow = (int64_t)t.q_row0 + qi;
@@ -60,7 +65,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   // Q^T operand (B of S^T = K Q^T): lane holds query qi, d = 16*ks + 8*hf .. +7
   bf16x8 qreg[D / 16];
   {
-    const uint16_t* qp = p.q + qrow * qstride + head * D + hf * 8;
+    const uint16_t* qp = qsrc + qrow * qstride + head * D + hf * 8;
 #pragma unroll
     for (int ks = 0; ks < D / 16; ++ks)
       qreg[ks] = as_bf16x8(qvalid ? ldg16(qp + ks * 16) : make_uint4(0, 0, 0, 0));
@@ -86,7 +91,7 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
     const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
-    const uint16_t* src = val ? (isB ? p.vb : p.va) : (isB ? p.kb : p.ka);
+    const uint16_t* src = val ? (isB ? vb : p.va) : (isB ? kb : p.ka);
     cp.issue(dst, src, row0, min(BN, len - kb0), kvstride, kvh * D);
   };
 
@@ -222,6 +227,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   if (qvalid) {
     const float inv = 1.f / l_tot;
     const int64_t obase = qrow * qstride + head * D;
+    const bool part1 = (t.flags & QT_PART1) != 0;
+    float* const o32 = p.o32 + (part1 ? p.o32_part : 0);
+    uint16_t* const o16 = prow ? p.o[1] : p.o[0];
 #pragma unroll
     for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
@@ -230,16 +238,27 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
         const float v0 = oacc[db][g4 * 4 + 0] * inv, v1 = oacc[db][g4 * 4 + 1] * inv;
         const float v2 = oacc[db][g4 * 4 + 2] * inv, v3 = oacc[db][g4 * 4 + 3] * inv;
         if constexpr (OUT32) {
-          *reinterpret_cast<float4*>(p.o32 + obase + d0) = make_float4(v0, v1, v2, v3);
+          *reinterpret_cast<float4*>(o32 + obase + d0) = make_float4(v0, v1, v2, v3);
         } else {
           typedef __bf16 bf16x4 __attribute__((ext_vector_type(4)));
           bf16x4 w;
           w[0] = (__bf16)v0; w[1] = (__bf16)v1; w[2] = (__bf16)v2; w[3] = (__bf16)v3;
-          *reinterpret_cast<bf16x4*>(p.o + obase + d0) = w;
+          *reinterpret_cast<bf16x4*>(o16 + obase + d0) = w;
         }
       }
     }
-    if (hf == 0) p.lse[(int64_t)head * p.lse_rows + qrow] = (m_run * c + __log2f(l_tot)) * kLn2;
+    if (hf == 0) {
+      float* lse;
+      int64_t lrows;
+      if constexpr (OUT32) {
+        lse = p.lse[0] + (part1 ? p.lse_part : 0);
+        lrows = p.lse_rows[0];
+      } else {
+        lse = prow ? p.lse[1] : p.lse[0];
+        lrows = prow ? p.lse_rows[1] : p.lse_rows[0];
+      }
+      lse[(int64_t)head * lrows + qrow] = (m_run * c + __log2f(l_tot)) * kLn2;
+    }
   }
 }
 

@@ -151,7 +151,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 
 int64_t qtile_cost(const QTile& t) { return (int64_t)t.q_len * (t.a_len + t.b_len); }
-int64_t kvtile_cost(const KVTile& t) { return (int64_t)t.q_len * t.kv_len; }
+int64_t kvtile_cost(const KVTile& t) { return (int64_t)(t.x_len + t.y_len) * t.kv_len; }
 
 // Tile order. Each XCD runs the tiles of one KV head in list order, so
 // concurrent workgroups share a K/V or Q/dO block in the XCD's L2 only when
@@ -211,10 +211,21 @@ void sort_segment_major(std::vector<T>& v, const std::vector<int>& seg, F cost, 
 int conc_qtiles(const Shape& s) { return std::max(1, 2 * 256 / s.hq); }
 int conc_kvtiles(const Shape& s) { return std::max(1, 256 / s.hkv); }
 
-// prompt causal tiles (prefill fwd and dQ)
-std::vector<QTile> prefill_qtiles(const Shape& s, int bm) {
-  std::vector<QTile> v;
+// Tile lists are built by appending (tile, segment id) pairs and sorted once
+// per launch. Segment ids: a group's prompt rows or prompt keys = g, branch b
+// = num_groups + b.
+template <class T>
+struct TileList {
+  std::vector<T> v;
   std::vector<int> seg;
+  void add(const T& t, int s) {
+    v.push_back(t);
+    seg.push_back(s);
+  }
+};
+
+// prompt causal query tiles (prefill fwd and dQ)
+void add_prefill_qtiles(TileList<QTile>& L, const Shape& s, int bm) {
   for (int g = 0; g < s.ng; ++g) {
     const int P = s.cp[g + 1] - s.cp[g];
     for (int t0 = 0; t0 < P; t0 += bm) {
@@ -224,22 +235,19 @@ std::vector<QTile> prefill_qtiles(const Shape& s, int bm) {
       t.b_row0 = s.cp[g];
       t.b_len = t0 + t.q_len;
       t.b_qpos = t0;
-      v.push_back(t);
-      seg.push_back(g);
+      t.flags = QT_PROMPT_ROWS;
+      L.add(t, g);
     }
   }
-  sort_segment_major(v, seg, qtile_cost, conc_qtiles(s));
-  return v;
 }
 
-// response tiles: part 0 = prompt keys only (spans the group's branches),
-// part 1 = own-branch causal keys only, fused = both
+// response query tiles: RP_PROMPT = prompt keys only (spans the group's
+// branches; first partial slot), RP_OWN = own-branch causal keys only (second
+// partial slot), RP_FUSED = both
 enum { RP_PROMPT = 0, RP_OWN = 1, RP_FUSED = 2 };
 
 // `keep` (optional, one flag per group) limits the tiles to the flagged groups
-std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which, const std::vector<char>* keep = nullptr) {
-  std::vector<QTile> v;
-  std::vector<int> seg;  // prompt partial: the group; otherwise the branch
+void add_replay_qtiles(TileList<QTile>& L, const Shape& s, int bm, int which, const std::vector<char>* keep = nullptr) {
   for (int g = 0; g < s.ng; ++g) {
     if (keep && !(*keep)[g]) continue;
     const int P = s.cp[g + 1] - s.cp[g];
@@ -251,8 +259,7 @@ std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which, const std::v
         t.q_len = std::min(bm, r1 - q0);
         t.a_row0 = s.cp[g];
         t.a_len = P;
-        v.push_back(t);
-        seg.push_back(g);
+        L.add(t, g);
       }
       continue;
     }
@@ -265,17 +272,16 @@ std::vector<QTile> replay_qtiles(const Shape& s, int bm, int which, const std::v
         if (which == RP_FUSED) {
           t.a_row0 = s.cp[g];
           t.a_len = P;
+        } else {
+          t.flags = QT_PART1;
         }
         t.b_row0 = s.cr[b];
         t.b_len = t0 + t.q_len;
         t.b_qpos = t0;
-        v.push_back(t);
-        seg.push_back(b);
+        L.add(t, s.ng + b);
       }
     }
   }
-  sort_segment_major(v, seg, qtile_cost, conc_qtiles(s));
-  return v;
 }
 
 // Replay forward mode per group (AUGTREE_REPLAY_AUTO). A mode's cost is the
@@ -314,142 +320,179 @@ std::vector<char> replay_split_groups(const Shape& s, int mode) {
   return v;
 }
 
-// causal key tiles over contiguous segments [start, start+len), segment id `id`
-void causal_kvtiles(std::vector<KVTile>& v, std::vector<int>& seg, int id, int32_t start, int32_t len, int bn) {
-  for (int k0 = 0; k0 < len; k0 += bn) {
-    seg.push_back(id);
+// prompt key tiles of every group: X = response rows r0 + x0 .. r0 + x1 - 1
+// of the group (all branches; every prompt key visible), Y = the prefill rows
+// from the tile's first key (causal) if `prefill`
+void add_prompt_kvtiles(TileList<KVTile>& L, const Shape& s, int bn, int g, int x0, int x1, bool prefill,
+                        int32_t flags) {
+  const int P = s.cp[g + 1] - s.cp[g];
+  // (a prefill-only call passes no branch offsets and an empty X range)
+  const int r0 = x1 > x0 ? s.cr[s.cb[g]] : 0;
+  for (int k0 = 0; k0 < P; k0 += bn) {
     KVTile t{};
-    t.kv_row0 = start + k0;
-    t.kv_len = std::min(bn, len - k0);
-    t.q_row0 = start + k0;  // queries before the first key cannot see it
-    t.q_len = len - k0;
-    t.causal = 1;
+    t.kv_row0 = s.cp[g] + k0;
+    t.kv_len = std::min(bn, P - k0);
+    t.x_row0 = r0 + x0;
+    t.x_len = x1 - x0;
+    if (prefill) {
+      t.y_row0 = s.cp[g] + k0;  // queries before the first key cannot see it
+      t.y_len = P - k0;
+    }
     t.kpos0 = k0;
-    t.qpos0 = k0;
-    v.push_back(t);
+    t.flags = flags | KV_PROMPT_KEYS;
+    L.add(t, g);
   }
 }
 
-std::vector<KVTile> prefill_kvtiles(const Shape& s, int bn) {
-  std::vector<KVTile> v;
-  std::vector<int> seg;
-  for (int g = 0; g < s.ng; ++g) causal_kvtiles(v, seg, g, s.cp[g], s.cp[g + 1] - s.cp[g], bn);
-  sort_segment_major(v, seg, kvtile_cost, conc_kvtiles(s));
-  return v;
-}
-
-std::vector<KVTile> response_kvtiles(const Shape& s, int bn) {
-  std::vector<KVTile> v;
-  std::vector<int> seg;
-  for (int b = 0; b < s.nb; ++b) causal_kvtiles(v, seg, b, s.cr[b], s.cr[b + 1] - s.cr[b], bn);
-  sort_segment_major(v, seg, kvtile_cost, conc_kvtiles(s));
-  return v;
-}
-
-// prompt keys x every response row of the group, rows cut into n_seed chunks
-std::vector<KVTile> seed_kvtiles(const Shape& s, int bn, int n_seed, int bq) {
-  std::vector<KVTile> v;
-  std::vector<int> seg;  // (group, chunk): the tiles of one segment sweep the same rows
-  for (int g = 0; g < s.ng; ++g) {
-    const int P = s.cp[g + 1] - s.cp[g];
-    const int r0 = s.cr[s.cb[g]], r1 = s.cr[s.cb[g + 1]];
-    const int64_t nr = r1 - r0;
-    for (int c = 0; c < n_seed; ++c) {
-      // chunk boundaries on multiples of the query block where possible
-      auto edge = [&](int k) -> int {
-        if (k == 0) return 0;
-        if (k == n_seed) return (int)nr;
-        int64_t e = nr * k / n_seed;
-        e = (e / bq) * bq;
-        return (int)std::min<int64_t>(e, nr);
-      };
-      const int c0 = edge(c), c1 = std::max(edge(c + 1), c0);
-      for (int k0 = 0; k0 < P; k0 += bn) {
-        KVTile t{};
-        t.kv_row0 = s.cp[g] + k0;
-        t.kv_len = std::min(bn, P - k0);
-        t.q_row0 = r0 + c0;
-        t.q_len = c1 - c0;
-        t.causal = 0;
-        t.part = c;
-        v.push_back(t);
-        seg.push_back(g * n_seed + c);
-      }
+// own-branch causal key tiles of every branch
+void add_response_kvtiles(TileList<KVTile>& L, const Shape& s, int bn) {
+  for (int b = 0; b < s.nb; ++b) {
+    const int R = s.cr[b + 1] - s.cr[b];
+    for (int k0 = 0; k0 < R; k0 += bn) {
+      KVTile t{};
+      t.kv_row0 = s.cr[b] + k0;
+      t.kv_len = std::min(bn, R - k0);
+      t.x_row0 = s.cr[b] + k0;
+      t.x_len = R - k0;
+      t.kpos0 = k0;
+      t.flags = KV_X_CAUSAL | KV_OUT_BF16;
+      L.add(t, s.ng + b);
     }
   }
-  sort_segment_major(v, seg, kvtile_cost, conc_kvtiles(s));
-  return v;
 }
 
-// ---------------------------------------------------------------------------- workspace layout
+// Boundaries of chunk c of n of a group's `nr` response rows, on multiples of
+// the query block where possible.
+int seed_edge(int64_t nr, int k, int n, int bq) {
+  if (k == 0) return 0;
+  if (k == n) return (int)nr;
+  int64_t e = nr * k / n;
+  e = (e / bq) * bq;
+  return (int)std::min<int64_t>(e, nr);
+}
+
+// ---------------------------------------------------------------------------- plans and workspace
 
 constexpr size_t kAlign = 256;
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
+// The launches of one entry point: up to three query-tile lists and one
+// key-tile list, each sorted for its launch. Lists longer than kInlineTiles
+// are uploaded to the start of the workspace (one copy); shorter ones travel
+// in the kernel arguments. The workspace then holds D = rowsum(dO * O) for
+// the backward ([Hq, T_P] then [Hq, T_R]).
 struct Plan {
-  std::vector<QTile> q1, q2, q3;  // forward / dQ tiles (split: q1 prompt, q2 own; auto: q3 fused groups)
-  std::vector<KVTile> kv1, kv2;   // dK/dV tiles
-  size_t off_q1 = 0, off_q2 = 0, off_q3 = 0, off_kv1 = 0, off_kv2 = 0, off_dsum = 0, bytes = 0;
-  int64_t dsum_rows = 0;
-  std::vector<char> blob;         // schedule bytes copied to the start of the workspace
-  size_t blob_bytes = 0;
+  TileList<QTile> q[3];
+  TileList<KVTile> kv;
+  size_t off_q[3] = {0, 0, 0}, off_kv = 0, off_dsum_p = 0, off_dsum_r = 0, bytes = 0, blob_bytes = 0;
+  int64_t dsum_rows_p = 0, dsum_rows_r = 0;
+  std::vector<char> blob;
 
+  void sort(const Shape& s) {
+    for (auto& l : q) sort_segment_major(l.v, l.seg, qtile_cost, conc_qtiles(s));
+    sort_segment_major(kv.v, kv.seg, kvtile_cost, conc_kvtiles(s));
+  }
+  // every list gets room in the workspace (its size does not depend on
+  // which lists end up inline)
   void layout(int hq) {
     size_t o = 0;
-    off_q1 = o; o = align_up(o + q1.size() * sizeof(QTile));
-    off_q2 = o; o = align_up(o + q2.size() * sizeof(QTile));
-    off_q3 = o; o = align_up(o + q3.size() * sizeof(QTile));
-    off_kv1 = o; o = align_up(o + kv1.size() * sizeof(KVTile));
-    off_kv2 = o; o = align_up(o + kv2.size() * sizeof(KVTile));
+    for (int i = 0; i < 3; ++i) {
+      off_q[i] = o;
+      o = align_up(o + q[i].v.size() * sizeof(QTile));
+    }
+    off_kv = o;
+    o = align_up(o + kv.v.size() * sizeof(KVTile));
     blob_bytes = o;
-    off_dsum = o; o = align_up(o + (size_t)dsum_rows * hq * sizeof(float));
+    off_dsum_p = o;
+    o = align_up(o + (size_t)dsum_rows_p * hq * sizeof(float));
+    off_dsum_r = o;
+    o = align_up(o + (size_t)dsum_rows_r * hq * sizeof(float));
     bytes = std::max<size_t>(o, kAlign);
   }
+  static bool inline_list(size_t n) { return n <= (size_t)kInlineTiles; }
+  // bytes of the workspace prefix that must be uploaded (0: every list inline)
+  size_t upload_bytes() const {
+    size_t end = 0;
+    for (int i = 0; i < 3; ++i)
+      if (!inline_list(q[i].v.size())) end = off_q[i] + q[i].v.size() * sizeof(QTile);
+    if (!inline_list(kv.v.size())) end = off_kv + kv.v.size() * sizeof(KVTile);
+    return end;
+  }
   void pack() {
-    blob.assign(blob_bytes, 0);
-    if (!q1.empty()) std::memcpy(blob.data() + off_q1, q1.data(), q1.size() * sizeof(QTile));
-    if (!q2.empty()) std::memcpy(blob.data() + off_q2, q2.data(), q2.size() * sizeof(QTile));
-    if (!q3.empty()) std::memcpy(blob.data() + off_q3, q3.data(), q3.size() * sizeof(QTile));
-    if (!kv1.empty()) std::memcpy(blob.data() + off_kv1, kv1.data(), kv1.size() * sizeof(KVTile));
-    if (!kv2.empty()) std::memcpy(blob.data() + off_kv2, kv2.data(), kv2.size() * sizeof(KVTile));
+    blob.assign(upload_bytes(), 0);
+    for (int i = 0; i < 3; ++i)
+      if (!inline_list(q[i].v.size()))
+        std::memcpy(blob.data() + off_q[i], q[i].v.data(), q[i].v.size() * sizeof(QTile));
+    if (!inline_list(kv.v.size())) std::memcpy(blob.data() + off_kv, kv.v.data(), kv.v.size() * sizeof(KVTile));
   }
 };
 
+// Points the launch parameters at list i: the workspace copy, or the kernel
+// arguments' inline copy.
+template <class P, class T>
+void bind_tiles(P& p, const TileList<T>& L, void* ws, size_t off) {
+  if (Plan::inline_list(L.v.size())) {
+    p.tiles = nullptr;
+    std::copy(L.v.begin(), L.v.end(), p.inl);
+  } else {
+    p.tiles = reinterpret_cast<const T*>(static_cast<char*>(ws) + off);
+  }
+}
+
+// Operation codes of augtree_workspace_size beyond the public four.
 Plan plan_for(const Shape& s, int op, int arg) {
   Plan pl;
+  const int bm = fwd_block_m(), bn = dkv_block_n(), bq = dkv_block_q();
   switch (op) {
     case AUGTREE_OP_PREFILL_FWD:
-      pl.q1 = prefill_qtiles(s, fwd_block_m());
+      add_prefill_qtiles(pl.q[0], s, bm);
       break;
     case AUGTREE_OP_REPLAY_FWD:
-      if (arg == AUGTREE_REPLAY_SPLIT) {
-        pl.q1 = replay_qtiles(s, fwd_block_m(), RP_PROMPT);
-        pl.q2 = replay_qtiles(s, fwd_block_m(), RP_OWN);
-      } else if (arg == AUGTREE_REPLAY_AUTO) {
-        const std::vector<char> split = replay_split_groups(s, arg);
-        std::vector<char> fused(split.size());
-        for (size_t g = 0; g < split.size(); ++g) fused[g] = !split[g];
-        pl.q1 = replay_qtiles(s, fwd_block_m(), RP_PROMPT, &split);
-        pl.q2 = replay_qtiles(s, fwd_block_m(), RP_OWN, &split);
-        pl.q3 = replay_qtiles(s, fwd_block_m(), RP_FUSED, &fused);
-      } else {
-        pl.q1 = replay_qtiles(s, fwd_block_m(), RP_FUSED);
-      }
+    case AUGTREE_OP_TREE_FWD: {
+      // q[0]: the bf16 launch (prefill tiles for the tree call, fused groups);
+      // q[1]: the split groups' partial tiles (fp32 launch)
+      if (op == AUGTREE_OP_TREE_FWD) add_prefill_qtiles(pl.q[0], s, bm);
+      const std::vector<char> split = replay_split_groups(s, arg);
+      std::vector<char> fused(split.size());
+      for (size_t g = 0; g < split.size(); ++g) fused[g] = !split[g];
+      add_replay_qtiles(pl.q[0], s, bm, RP_FUSED, &fused);
+      add_replay_qtiles(pl.q[1], s, bm, RP_PROMPT, &split);
+      add_replay_qtiles(pl.q[1], s, bm, RP_OWN, &split);
       break;
+    }
     case AUGTREE_OP_PREFILL_BWD:
-      pl.q1 = prefill_qtiles(s, dq_block_m());
-      pl.kv1 = prefill_kvtiles(s, dkv_block_n());
-      pl.dsum_rows = s.tp;
+      add_prefill_qtiles(pl.q[0], s, dq_block_m());
+      for (int g = 0; g < s.ng; ++g) add_prompt_kvtiles(pl.kv, s, bn, g, 0, 0, true, KV_OUT_SLAB);
+      pl.dsum_rows_p = s.tp;
       break;
     case AUGTREE_OP_REPLAY_BWD:
-      pl.q1 = replay_qtiles(s, dq_block_m(), RP_FUSED);
-      pl.kv1 = response_kvtiles(s, dkv_block_n());
-      pl.kv2 = seed_kvtiles(s, dkv_block_n(), arg, dkv_block_q());
-      pl.dsum_rows = s.tr;
+      add_replay_qtiles(pl.q[0], s, dq_block_m(), RP_FUSED);
+      add_response_kvtiles(pl.kv, s, bn);
+      for (int g = 0; g < s.ng; ++g) {
+        const int64_t nr = s.cr[s.cb[g + 1]] - s.cr[s.cb[g]];
+        for (int c = 0; c < arg; ++c) {
+          const int c0 = seed_edge(nr, c, arg, bq), c1 = std::max(seed_edge(nr, c + 1, arg, bq), c0);
+          add_prompt_kvtiles(pl.kv, s, bn, g, c0, c1, false, KV_OUT_SLAB | (c << KV_PART_SHIFT));
+        }
+      }
+      pl.dsum_rows_r = s.tr;
       break;
+    case AUGTREE_OP_TREE_BWD: {
+      add_prefill_qtiles(pl.q[0], s, dq_block_m());
+      add_replay_qtiles(pl.q[0], s, dq_block_m(), RP_FUSED);
+      add_response_kvtiles(pl.kv, s, bn);
+      // arg != 0: the fp32 copy of the prompt-key gradient is requested too
+      const int32_t out = KV_OUT_BF16 | (arg ? KV_OUT_SLAB : 0);
+      for (int g = 0; g < s.ng; ++g)
+        add_prompt_kvtiles(pl.kv, s, bn, g, 0, s.cr[s.cb[g + 1]] - s.cr[s.cb[g]], true, out);
+      pl.dsum_rows_p = s.tp;
+      pl.dsum_rows_r = s.tr;
+      break;
+    }
     default:
       break;
   }
+  pl.sort(s);
   pl.layout(s.hq);
   return pl;
 }
@@ -464,8 +507,8 @@ int check_ws(const Plan& pl, void* ws, size_t ws_bytes) {
 
 int upload(Plan& pl, void* ws, hipStream_t stream) {
   pl.pack();
-  if (pl.blob_bytes == 0) return AUGTREE_OK;
-  const hipError_t e = hipMemcpyAsync(ws, pl.blob.data(), pl.blob_bytes, hipMemcpyHostToDevice, stream);
+  if (pl.blob.empty()) return AUGTREE_OK;
+  const hipError_t e = hipMemcpyAsync(ws, pl.blob.data(), pl.blob.size(), hipMemcpyHostToDevice, stream);
   if (e != hipSuccess) return fail(AUGTREE_ERR_HIP, "schedule copy: %s", hipGetErrorString(e));
   return AUGTREE_OK;
 }
@@ -475,12 +518,111 @@ int hip_status(hipError_t e, const char* what) {
   return AUGTREE_OK;
 }
 
-template <class T>
-const T* at(void* ws, size_t off) {
-  return reinterpret_cast<const T*>(static_cast<char*>(ws) + off);
+float log2e_scale(float s) { return s * kLog2e; }
+
+// ---------------------------------------------------------------------------- launch sequences
+
+// Tensors of one forward or backward call (any may be null where unused).
+struct Tensors {
+  const uint16_t *q_p, *k_p, *v_p, *o_p, *do_p;
+  const float* lse_p;
+  const uint16_t *q_r, *k_r, *v_r, *o_r, *do_r;
+  const float* lse_r;
+};
+
+// Forward launches of a plan: q[0] (bf16 outputs), q[1] (split partials,
+// fp32) and the merge of the split groups' rows.
+int run_fwd(const Shape& s, const Plan& pl, int mode, const Tensors& x, uint16_t* o_p, float* lse_p, uint16_t* o_r,
+            float* lse_r, float* o_part, float* lse_part, void* ws, hipStream_t str, const char* role_main) {
+  int st;
+  FwdParams p{};
+  p.q[0] = x.q_r; p.q[1] = x.q_p;
+  p.ka = x.k_p; p.va = x.v_p;
+  p.kb[0] = x.k_r; p.vb[0] = x.v_r; p.kb[1] = x.k_p; p.vb[1] = x.v_p;
+  p.o[0] = o_r; p.o[1] = o_p;
+  p.lse[0] = lse_r; p.lse[1] = lse_p;
+  p.lse_rows[0] = s.tr; p.lse_rows[1] = s.tp;
+  p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d;
+  p.scale_log2 = log2e_scale(s.scale);
+  if (!pl.q[0].v.empty()) {
+    bind_tiles(p, pl.q[0], ws, pl.off_q[0]);
+    HookScope h(role_main, str);
+    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q[0].v.size(), false, str), "forward launch"))) return st;
+  }
+  if (pl.q[1].v.empty()) return AUGTREE_OK;
+  // split groups: both partial states in one launch, then the merge
+  bind_tiles(p, pl.q[1], ws, pl.off_q[1]);
+  p.o32 = o_part; p.o32_part = s.tr * s.hq * s.d;
+  p.lse[0] = lse_part; p.lse_part = s.tr * s.hq;
+  {
+    HookScope h("fwd_replay_split", str);
+    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q[1].v.size(), true, str), "split partial launch"))) return st;
+  }
+  const std::vector<char> split = replay_split_groups(s, mode);
+  for (int g = 0; g < s.ng;) {  // one merge per run of consecutive split groups (contiguous rows)
+    if (!split[g]) { ++g; continue; }
+    int g1 = g;
+    while (g1 < s.ng && split[g1]) ++g1;
+    const int64_t r0 = s.cr[s.cb[g]], r1 = s.cr[s.cb[g1]];
+    HookScope h("lse_merge", str);
+    if ((st = hip_status(launch_lse_merge(r0, r1 - r0, s.tr, s.hq, s.d, 2, o_part, lse_part, o_r, nullptr, lse_r, str),
+                         "lse merge launch")))
+      return st;
+    g = g1;
+  }
+  return AUGTREE_OK;
 }
 
-float log2e_scale(float s) { return s * kLog2e; }
+// Backward launches of a plan: the dQ kernel (which also forms D into the
+// workspace), then the dK/dV kernel that reads D.
+struct BwdOut {
+  uint16_t *dq_p, *dq_r;
+  float* dq_p32;
+  uint16_t *dk_p, *dv_p, *dk_r, *dv_r;
+  float* slab;
+  int64_t slab_rows;
+};
+
+int run_bwd(const Shape& s, const Plan& pl, const Tensors& x, const BwdOut& out, void* ws, hipStream_t str,
+            const char* role_dq, const char* role_dkv) {
+  int st;
+  float* dsum_p = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_dsum_p);
+  float* dsum_r = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_dsum_r);
+  const float sl2 = log2e_scale(s.scale);
+  if (!pl.q[0].v.empty()) {
+    DqParams p{};
+    bind_tiles(p, pl.q[0], ws, pl.off_q[0]);
+    p.q[0] = x.q_r; p.q[1] = x.q_p;
+    p.dout[0] = x.do_r; p.dout[1] = x.do_p;
+    p.o[0] = x.o_r; p.o[1] = x.o_p;
+    p.lse[0] = x.lse_r; p.lse[1] = x.lse_p;
+    p.dsum[0] = dsum_r; p.dsum[1] = dsum_p;
+    p.lse_rows[0] = s.tr; p.lse_rows[1] = s.tp;
+    p.ka = x.k_p; p.va = x.v_p;
+    p.kb[0] = x.k_r; p.vb[0] = x.v_r; p.kb[1] = x.k_p; p.vb[1] = x.v_p;
+    p.dq[0] = out.dq_r; p.dq[1] = out.dq_p;
+    p.dq32[1] = out.dq_p32;
+    p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
+    HookScope h(role_dq, str);
+    if ((st = hip_status(launch_attn_dq(p, (int)pl.q[0].v.size(), str), "dq launch"))) return st;
+  }
+  if (!pl.kv.v.empty()) {
+    DkvParams p{};
+    bind_tiles(p, pl.kv, ws, pl.off_kv);
+    p.k[0] = x.k_r; p.v[0] = x.v_r; p.k[1] = x.k_p; p.v[1] = x.v_p;
+    p.q[0] = x.q_r; p.q[1] = x.q_p;
+    p.dout[0] = x.do_r; p.dout[1] = x.do_p;
+    p.lse[0] = x.lse_r; p.lse[1] = x.lse_p;
+    p.dsum[0] = dsum_r; p.dsum[1] = dsum_p;
+    p.lse_rows[0] = s.tr; p.lse_rows[1] = s.tp;
+    p.dk[0] = out.dk_r; p.dv[0] = out.dv_r; p.dk[1] = out.dk_p; p.dv[1] = out.dv_p;
+    p.slab = out.slab; p.slab_rows = out.slab_rows;
+    p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
+    HookScope h(role_dkv, str);
+    if ((st = hip_status(launch_attn_dkv(p, (int)pl.kv.v.size(), str), "dkv launch"))) return st;
+  }
+  return AUGTREE_OK;
+}
 
 }  // namespace
 
@@ -519,12 +661,12 @@ size_t augtree_workspace_size(const augtree_groups* grp, int op, int arg) {
   Shape s;
   const bool prefill_only = op == AUGTREE_OP_PREFILL_FWD || op == AUGTREE_OP_PREFILL_BWD;
   if (validate_groups(grp, &s, !prefill_only) != AUGTREE_OK) return 0;
-  if (op < AUGTREE_OP_PREFILL_FWD || op > AUGTREE_OP_REPLAY_BWD) {
+  if (op < AUGTREE_OP_PREFILL_FWD || op > AUGTREE_OP_TREE_BWD) {
     fail(AUGTREE_ERR_INVALID_ARGUMENT, "unknown op %d", op);
     return 0;
   }
-  if (op == AUGTREE_OP_REPLAY_FWD && arg != AUGTREE_REPLAY_FUSED && arg != AUGTREE_REPLAY_SPLIT &&
-      arg != AUGTREE_REPLAY_AUTO) {
+  if ((op == AUGTREE_OP_REPLAY_FWD || op == AUGTREE_OP_TREE_FWD) && arg != AUGTREE_REPLAY_FUSED &&
+      arg != AUGTREE_REPLAY_SPLIT && arg != AUGTREE_REPLAY_AUTO) {
     fail(AUGTREE_ERR_INVALID_ARGUMENT, "unknown replay mode %d", arg);
     return 0;
   }
@@ -532,6 +674,7 @@ size_t augtree_workspace_size(const augtree_groups* grp, int op, int arg) {
     fail(AUGTREE_ERR_INVALID_ARGUMENT, "n_seed %d not in [1,64]", arg);
     return 0;
   }
+  if (op == AUGTREE_OP_TREE_BWD) arg = 1;  // room for the largest schedule (fp32 prompt copy or not)
   ok();
   return plan_for(s, op, arg).bytes;
 }
@@ -547,16 +690,11 @@ int augtree_prefill_fwd(const augtree_groups* grp, const uint16_t* q_p, const ui
   if ((st = check_device_impl())) return st;
   hipStream_t str = static_cast<hipStream_t>(stream);
   if ((st = upload(pl, ws, str))) return st;
-  FwdParams p{};
-  p.tiles = at<QTile>(ws, pl.off_q1);
-  p.q = q_p; p.ka = k_p; p.va = v_p; p.kb = k_p; p.vb = v_p;
-  p.o = o_p; p.lse = lse_p; p.lse_rows = s.tp;
-  p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d;
-  p.scale_log2 = log2e_scale(s.scale);
-  {
-    HookScope h("fwd_prefill", str);
-    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), false, str), "prefill fwd launch"))) return st;
-  }
+  Tensors x{};
+  x.q_p = q_p; x.k_p = k_p; x.v_p = v_p;
+  if ((st = run_fwd(s, pl, AUGTREE_REPLAY_FUSED, x, o_p, lse_p, nullptr, nullptr, nullptr, nullptr, ws, str,
+                    "fwd_prefill")))
+    return st;
   return ok();
 }
 
@@ -576,50 +714,32 @@ int augtree_replay_fwd(const augtree_groups* grp, int mode, const uint16_t* q_r,
   if ((st = check_device_impl())) return st;
   hipStream_t str = static_cast<hipStream_t>(stream);
   if ((st = upload(pl, ws, str))) return st;
-  FwdParams p{};
-  p.q = q_r; p.ka = k_p; p.va = v_p; p.kb = k_r; p.vb = v_r;
-  p.lse_rows = s.tr;
-  p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d;
-  p.scale_log2 = log2e_scale(s.scale);
-  // fused tiles: all groups (FUSED) or the groups the cost rule keeps fused (AUTO)
-  const std::vector<QTile>& fused_tiles = mode == AUGTREE_REPLAY_FUSED ? pl.q1 : pl.q3;
-  const size_t fused_off = mode == AUGTREE_REPLAY_FUSED ? pl.off_q1 : pl.off_q3;
-  if (!fused_tiles.empty()) {
-    p.tiles = at<QTile>(ws, fused_off);
-    p.o = o_r; p.lse = lse_r;
-    HookScope h("fwd_replay", str);
-    if ((st = hip_status(launch_attn_fwd(p, (int)fused_tiles.size(), false, str), "replay fwd launch"))) return st;
-  }
-  if (mode == AUGTREE_REPLAY_FUSED) return ok();
-  // split groups: two partial states, then the merge over their rows
-  const int64_t part_o = s.tr * s.hq * s.d;
-  const int64_t part_l = s.tr * s.hq;
-  p.o = nullptr;
-  if (!pl.q1.empty()) {
-    p.tiles = at<QTile>(ws, pl.off_q1);
-    p.o32 = o_part; p.lse = lse_part;
-    HookScope h("fwd_replay_prompt", str);
-    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q1.size(), true, str), "replay prompt partial launch"))) return st;
-  }
-  if (!pl.q2.empty()) {
-    p.tiles = at<QTile>(ws, pl.off_q2);
-    p.o32 = o_part + part_o; p.lse = lse_part + part_l;
-    HookScope h("fwd_replay_own", str);
-    if ((st = hip_status(launch_attn_fwd(p, (int)pl.q2.size(), true, str), "replay own partial launch"))) return st;
-  }
-  const std::vector<char> split = replay_split_groups(s, mode);
-  for (int g = 0; g < s.ng;) {  // one merge per run of consecutive split groups (contiguous rows)
-    if (!split[g]) { ++g; continue; }
-    int g1 = g;
-    while (g1 < s.ng && split[g1]) ++g1;
-    const int64_t r0 = s.cr[s.cb[g]], r1 = s.cr[s.cb[g1]];
-    HookScope h("lse_merge", str);
-    if ((st = hip_status(launch_lse_merge(r0, r1 - r0, s.tr, s.hq, s.d, 2, o_part, lse_part, o_r, nullptr, lse_r,
-                                          str),
-                         "lse merge launch")))
-      return st;
-    g = g1;
-  }
+  Tensors x{};
+  x.k_p = k_p; x.v_p = v_p; x.q_r = q_r; x.k_r = k_r; x.v_r = v_r;
+  if ((st = run_fwd(s, pl, mode, x, nullptr, nullptr, o_r, lse_r, o_part, lse_part, ws, str, "fwd_replay")))
+    return st;
+  return ok();
+}
+
+int augtree_tree_fwd(const augtree_groups* grp, int mode, const uint16_t* q_p, const uint16_t* k_p,
+                     const uint16_t* v_p, const uint16_t* q_r, const uint16_t* k_r, const uint16_t* v_r, uint16_t* o_p,
+                     float* lse_p, uint16_t* o_r, float* lse_r, float* o_part, float* lse_part, void* ws,
+                     size_t ws_bytes, void* stream) {
+  Shape s;
+  int st = validate_groups(grp, &s);
+  if (st) return st;
+  if (mode != AUGTREE_REPLAY_FUSED && mode != AUGTREE_REPLAY_SPLIT && mode != AUGTREE_REPLAY_AUTO)
+    return fail(AUGTREE_ERR_INVALID_ARGUMENT, "unknown replay mode %d", mode);
+  REQUIRE_PTR(q_p); REQUIRE_PTR(k_p); REQUIRE_PTR(v_p); REQUIRE_PTR(q_r); REQUIRE_PTR(k_r); REQUIRE_PTR(v_r);
+  REQUIRE_PTR(o_p); REQUIRE_PTR(lse_p); REQUIRE_PTR(o_r); REQUIRE_PTR(lse_r);
+  if (mode != AUGTREE_REPLAY_FUSED) { REQUIRE_PTR(o_part); REQUIRE_PTR(lse_part); }
+  Plan pl = plan_for(s, AUGTREE_OP_TREE_FWD, mode);
+  if ((st = check_ws(pl, ws, ws_bytes))) return st;
+  if ((st = check_device_impl())) return st;
+  hipStream_t str = static_cast<hipStream_t>(stream);
+  if ((st = upload(pl, ws, str))) return st;
+  const Tensors x{q_p, k_p, v_p, nullptr, nullptr, nullptr, q_r, k_r, v_r, nullptr, nullptr, nullptr};
+  if ((st = run_fwd(s, pl, mode, x, o_p, lse_p, o_r, lse_r, o_part, lse_part, ws, str, "fwd_tree"))) return st;
   return ok();
 }
 
@@ -668,40 +788,13 @@ int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uin
   if ((st = check_device_impl())) return st;
   hipStream_t str = static_cast<hipStream_t>(stream);
   if ((st = upload(pl, ws, str))) return st;
-  float* dsum = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_dsum);
-  {
-    HookScope h("dsum_replay", str);
-    if ((st = hip_status(launch_bwd_dsum(o_r, do_r, dsum, s.tr, s.hq, s.d, str), "dsum launch"))) return st;
-  }
-  const float sl2 = log2e_scale(s.scale);
-  {  // prompt seeds: prompt keys x all response rows of the group (Eq. 2 sum in registers)
-    DkvParams p{};
-    p.tiles = at<KVTile>(ws, pl.off_kv2);
-    p.k = k_p; p.v = v_p; p.q = q_r; p.dout = do_r; p.lse = lse_r; p.dsum = dsum;
-    p.dkv32 = dkv_p_seed; p.out_rows = s.tp; p.lse_rows = s.tr;
-    p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
-    HookScope h("dkv_seed", str);
-    if ((st = hip_status(launch_attn_dkv(p, (int)pl.kv2.size(), true, str), "seed dkv launch"))) return st;
-  }
-  {  // own-branch keys, causal
-    DkvParams p{};
-    p.tiles = at<KVTile>(ws, pl.off_kv1);
-    p.k = k_r; p.v = v_r; p.q = q_r; p.dout = do_r; p.lse = lse_r; p.dsum = dsum;
-    p.dk = dk_r; p.dv = dv_r; p.out_rows = s.tr; p.lse_rows = s.tr;
-    p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
-    HookScope h("dkv_resp", str);
-    if ((st = hip_status(launch_attn_dkv(p, (int)pl.kv1.size(), false, str), "response dkv launch"))) return st;
-  }
-  {  // dQ over prompt keys then own-branch keys
-    DqParams p{};
-    p.tiles = at<QTile>(ws, pl.off_q1);
-    p.q = q_r; p.dout = do_r; p.lse = lse_r; p.dsum = dsum;
-    p.ka = k_p; p.va = v_p; p.kb = k_r; p.vb = v_r;
-    p.dq = dq_r; p.lse_rows = s.tr;
-    p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
-    HookScope h("dq_replay", str);
-    if ((st = hip_status(launch_attn_dq(p, (int)pl.q1.size(), str), "replay dq launch"))) return st;
-  }
+  Tensors x{};
+  x.k_p = k_p; x.v_p = v_p;
+  x.q_r = q_r; x.k_r = k_r; x.v_r = v_r; x.o_r = o_r; x.do_r = do_r; x.lse_r = lse_r;
+  BwdOut out{};
+  out.dq_r = dq_r; out.dk_r = dk_r; out.dv_r = dv_r;
+  out.slab = dkv_p_seed; out.slab_rows = s.tp;
+  if ((st = run_bwd(s, pl, x, out, ws, str, "dq_replay", "dkv_replay"))) return st;
   return ok();
 }
 
@@ -720,31 +813,38 @@ int augtree_prefill_bwd(const augtree_groups* grp, const uint16_t* q_p, const ui
   if ((st = check_device_impl())) return st;
   hipStream_t str = static_cast<hipStream_t>(stream);
   if ((st = upload(pl, ws, str))) return st;
-  float* dsum = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_dsum);
-  {
-    HookScope h("dsum_prefill", str);
-    if ((st = hip_status(launch_bwd_dsum(o_p, do_p, dsum, s.tp, s.hq, s.d, str), "dsum launch"))) return st;
-  }
-  const float sl2 = log2e_scale(s.scale);
-  {
-    DkvParams p{};
-    p.tiles = at<KVTile>(ws, pl.off_kv1);
-    p.k = k_p; p.v = v_p; p.q = q_p; p.dout = do_p; p.lse = lse_p; p.dsum = dsum;
-    p.dkv32 = dkv_p_self; p.out_rows = s.tp; p.lse_rows = s.tp;
-    p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
-    HookScope h("dkv_prefill", str);
-    if ((st = hip_status(launch_attn_dkv(p, (int)pl.kv1.size(), true, str), "prefill dkv launch"))) return st;
-  }
-  {
-    DqParams p{};
-    p.tiles = at<QTile>(ws, pl.off_q1);
-    p.q = q_p; p.dout = do_p; p.lse = lse_p; p.dsum = dsum;
-    p.ka = k_p; p.va = v_p; p.kb = k_p; p.vb = v_p;
-    p.dq = dq_p; p.dq32 = dq_p_f32; p.lse_rows = s.tp;
-    p.hq = s.hq; p.hkv = s.hkv; p.group = s.group; p.head_dim = s.d; p.scale = s.scale; p.scale_log2 = sl2;
-    HookScope h("dq_prefill", str);
-    if ((st = hip_status(launch_attn_dq(p, (int)pl.q1.size(), str), "prefill dq launch"))) return st;
-  }
+  Tensors x{};
+  x.q_p = q_p; x.k_p = k_p; x.v_p = v_p; x.o_p = o_p; x.do_p = do_p; x.lse_p = lse_p;
+  BwdOut out{};
+  out.dq_p = dq_p; out.dq_p32 = dq_p_f32;
+  out.slab = dkv_p_self; out.slab_rows = s.tp;
+  if ((st = run_bwd(s, pl, x, out, ws, str, "dq_prefill", "dkv_prefill"))) return st;
+  return ok();
+}
+
+int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p, const uint16_t* v_p,
+                     const uint16_t* o_p, const float* lse_p, const uint16_t* do_p, const uint16_t* q_r,
+                     const uint16_t* k_r, const uint16_t* v_r, const uint16_t* o_r, const float* lse_r,
+                     const uint16_t* do_r, uint16_t* dq_p, uint16_t* dk_p, uint16_t* dv_p, float* dkv_p_f32,
+                     uint16_t* dq_r, uint16_t* dk_r, uint16_t* dv_r, void* ws, size_t ws_bytes, void* stream) {
+  Shape s;
+  int st = validate_groups(grp, &s);
+  if (st) return st;
+  REQUIRE_PTR(q_p); REQUIRE_PTR(k_p); REQUIRE_PTR(v_p); REQUIRE_PTR(o_p); REQUIRE_PTR(lse_p); REQUIRE_PTR(do_p);
+  REQUIRE_PTR(q_r); REQUIRE_PTR(k_r); REQUIRE_PTR(v_r); REQUIRE_PTR(o_r); REQUIRE_PTR(lse_r); REQUIRE_PTR(do_r);
+  REQUIRE_PTR(dq_p); REQUIRE_PTR(dk_p); REQUIRE_PTR(dv_p); REQUIRE_PTR(dq_r); REQUIRE_PTR(dk_r); REQUIRE_PTR(dv_r);
+  OPTIONAL_PTR(dkv_p_f32);
+  Plan pl = plan_for(s, AUGTREE_OP_TREE_BWD, dkv_p_f32 ? 1 : 0);
+  if ((st = check_ws(pl, ws, ws_bytes))) return st;
+  if ((st = check_device_impl())) return st;
+  hipStream_t str = static_cast<hipStream_t>(stream);
+  if ((st = upload(pl, ws, str))) return st;
+  const Tensors x{q_p, k_p, v_p, o_p, do_p, lse_p, q_r, k_r, v_r, o_r, do_r, lse_r};
+  BwdOut out{};
+  out.dq_p = dq_p; out.dq_r = dq_r;
+  out.dk_p = dk_p; out.dv_p = dv_p; out.dk_r = dk_r; out.dv_r = dv_r;
+  out.slab = dkv_p_f32; out.slab_rows = s.tp;
+  if ((st = run_bwd(s, pl, x, out, ws, str, "dq_tree", "dkv_tree"))) return st;
   return ok();
 }
 

@@ -61,6 +61,19 @@ __device__ __forceinline__ bf16x8 to_bf16x8(const f32x16& v, int base) {
   return r;
 }
 
+// acc + the sum of the eight bf16 values of v, in fp32 (v_dot2c_f32_bf16
+// against ones: the products are exact).
+__device__ __forceinline__ float sum_bf16x8(const bf16x8& v, float acc) {
+  typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+  const bf16x2 one = {(__bf16)1.f, (__bf16)1.f};
+#pragma unroll
+  for (int j = 0; j < 4; ++j) {
+    const bf16x2 pair = {v[2 * j], v[2 * j + 1]};
+    acc = __builtin_amdgcn_fdot2_f32_bf16(pair, one, acc, false);
+  }
+  return acc;
+}
+
 // bf16 element e (0..7) of a 16-byte chunk, as the low 16 bits.
 __device__ __forceinline__ uint32_t half16(const uint4& v, int e) {
   uint32_t x;
@@ -271,6 +284,25 @@ __device__ __forceinline__ float pair_max(float x) {
 __device__ __forceinline__ float pair_sum(float x) {
   const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
   return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
+// ---------------------------------------------------------------------------- tile schedules
+
+// Tile `i` of a launch: from the device schedule when there is one, else
+// from the copy carried in the kernel arguments. Every field is made
+// wavefront-uniform (scalar registers), as a plain scalar load of the
+// schedule would leave it.
+template <class T>
+__device__ __forceinline__ T load_tile(const T* tiles, const T* inl, int i) {
+  static_assert(sizeof(T) == 32, "tile layout");
+  const T t = tiles ? tiles[i] : inl[i];
+  int32_t w[8];
+  __builtin_memcpy(w, &t, 32);
+#pragma unroll
+  for (int k = 0; k < 8; ++k) w[k] = __builtin_amdgcn_readfirstlane(w[k]);
+  T r;
+  __builtin_memcpy(&r, w, 32);
+  return r;
 }
 
 // ---------------------------------------------------------------------------- workgroup order

@@ -1,4 +1,9 @@
 // Host-callable launchers of the gfx950 kernels (internal to libaugtree).
+//
+// Arrays of two pointers are indexed by the kind of rows or keys a tile
+// covers: [0] response rows / branch keys, [1] prompt rows / prompt keys.
+// A launch of up to kInlineTiles tiles carries its schedule in the kernel
+// arguments (tiles == nullptr), so small launches need no schedule upload.
 #pragma once
 
 #include <hip/hip_runtime_api.h>
@@ -8,62 +13,68 @@
 
 namespace augtree {
 
+constexpr int kInlineTiles = 32;
+
 struct FwdParams {
-  const QTile* tiles;
-  const uint16_t* q;   // [rows, hq, d]
-  const uint16_t* ka;  // segment A keys/values [*, hkv, d]
+  const QTile* tiles;         // device schedule, or nullptr: `inl`
+  const uint16_t* q[2];       // [rows, hq, d]
+  const uint16_t* ka;         // segment A keys/values (prompt) [*, hkv, d]
   const uint16_t* va;
-  const uint16_t* kb;  // segment B keys/values
-  const uint16_t* vb;
-  uint16_t* o;         // bf16 output [rows, hq, d] (when out_f32 is false)
-  float* o32;          // fp32 output (when out_f32 is true)
-  float* lse;          // [hq, lse_rows]
-  int64_t lse_rows;
+  const uint16_t* kb[2];      // segment B keys/values of response / prompt rows
+  const uint16_t* vb[2];
+  uint16_t* o[2];             // bf16 outputs [rows, hq, d] (bf16 kernel)
+  float* o32;                 // fp32 partial outputs (fp32 kernel), slot 1 at + o32_part
+  int64_t o32_part;
+  float* lse[2];              // [hq, lse_rows]; fp32 kernel: lse[0], slot 1 at + lse_part
+  int64_t lse_rows[2];
+  int64_t lse_part;
   int hq, hkv, group, head_dim;
-  float scale_log2;    // softmax_scale * log2(e)
-  int n_units;         // tiles x KV heads (set by the launcher)
+  float scale_log2;           // softmax_scale * log2(e)
+  int n_units;                // tiles x KV heads (set by the launcher)
+  QTile inl[kInlineTiles];
 };
 
 struct DqParams {
   const QTile* tiles;
-  const uint16_t* q;
-  const uint16_t* dout;
-  const float* lse;    // natural-log LSE [hq, lse_rows]
-  const float* dsum;   // D = rowsum(dO * O) [hq, lse_rows]
+  const uint16_t* q[2];
+  const uint16_t* dout[2];
+  const uint16_t* o[2];       // forward output (bf16): D = rowsum(dO * O) is formed here
+  const float* lse[2];        // natural-log LSE [hq, lse_rows]
+  float* dsum[2];             // D written here [hq, lse_rows] (read by the dK/dV kernel)
+  int64_t lse_rows[2];
   const uint16_t* ka;
   const uint16_t* va;
-  const uint16_t* kb;
-  const uint16_t* vb;
-  uint16_t* dq;        // bf16 [rows, hq, d] (nullable)
-  float* dq32;         // fp32 (nullable)
-  int64_t lse_rows;
+  const uint16_t* kb[2];
+  const uint16_t* vb[2];
+  uint16_t* dq[2];            // bf16 [rows, hq, d] (nullable)
+  float* dq32[2];             // fp32 (nullable)
   int hq, hkv, group, head_dim;
   float scale, scale_log2;
-  int n_units;         // tiles x KV heads (set by the launcher)
+  int n_units;
+  QTile inl[kInlineTiles];
 };
 
 struct DkvParams {
   const KVTile* tiles;
-  const uint16_t* k;     // keys/values of the tile rows [*, hkv, d]
-  const uint16_t* v;
-  const uint16_t* q;     // queries [*, hq, d]
-  const uint16_t* dout;
-  const float* lse;      // [hq, lse_rows]
-  const float* dsum;     // [hq, lse_rows]
-  uint16_t* dk;          // bf16 outputs [*, hkv, d] (when out_f32 is false)
-  uint16_t* dv;
-  float* dkv32;          // fp32 slabs [part][2][out_rows, hkv, d] (when out_f32 is true)
-  int64_t out_rows;
-  int64_t lse_rows;
+  const uint16_t* k[2];       // keys/values [*, hkv, d]: [0] response, [1] prompt
+  const uint16_t* v[2];
+  const uint16_t* q[2];       // queries [*, hq, d]: [0] response rows, [1] prompt rows
+  const uint16_t* dout[2];
+  const float* lse[2];        // [hq, lse_rows]
+  const float* dsum[2];
+  int64_t lse_rows[2];
+  uint16_t* dk[2];            // bf16 outputs [*, hkv, d] (KV_OUT_BF16)
+  uint16_t* dv[2];
+  float* slab;                // fp32 slabs [part][2][slab_rows, hkv, d] (KV_OUT_SLAB)
+  int64_t slab_rows;
   int hq, hkv, group, head_dim;
   float scale, scale_log2;
+  KVTile inl[kInlineTiles];
 };
 
 hipError_t launch_attn_fwd(const FwdParams& p, int n_tiles, bool out_f32, hipStream_t stream);
 hipError_t launch_attn_dq(const DqParams& p, int n_tiles, hipStream_t stream);
-hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, bool out_f32, hipStream_t stream);
-hipError_t launch_bwd_dsum(const uint16_t* o, const uint16_t* dout, float* dsum, int64_t rows, int hq,
-                           int head_dim, hipStream_t stream);
+hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, hipStream_t stream);
 // rows row0 .. row0 + rows - 1 of [total_rows]-row tensors
 hipError_t launch_lse_merge(int64_t row0, int64_t rows, int64_t total_rows, int heads, int head_dim, int n_parts,
                             const float* o_parts, const float* lse_parts, uint16_t* o, float* o32, float* lse,

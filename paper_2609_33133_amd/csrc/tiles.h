@@ -9,25 +9,48 @@ constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
 // Query tile of the forward and dQ kernels: up to BM query rows, attending to
-// segment A (every key visible) and then segment B (causal: query i of the
-// tile sits at segment position b_qpos + i and sees keys 0 .. b_qpos + i).
+// segment A (prompt keys, every key visible) and then segment B (causal:
+// query i of the tile sits at segment position b_qpos + i and sees keys
+// 0 .. b_qpos + i).
 struct QTile {
   int32_t q_row0, q_len;
   int32_t a_row0, a_len;
   int32_t b_row0, b_len, b_qpos;
-  int32_t pad;
+  int32_t flags;  // QT_*
 };
 
-// Key tile of the dK/dV kernel: up to 128 keys of one KV head against a
-// range of query rows. Causal tiles: key j of the tile sits at position
-// kpos0 + j of its segment, query i of the range at qpos0 + i, visible iff
-// kpos0 + j <= qpos0 + i. Output rows are the key rows; fp32 outputs go to
-// slab `part`.
+enum : int32_t {
+  // the query rows are prompt rows (Q_P, O_P, LSE_P; segment B = prompt
+  // keys); otherwise response rows (Q_R, O_R, LSE_R; segment B = the
+  // branch's own keys)
+  QT_PROMPT_ROWS = 1,
+  // fp32 partial outputs: write the second partial slot (own-branch partial)
+  QT_PART1 = 2,
+};
+
+// Key tile of the dK/dV kernel: up to 128 keys of one KV head against up to
+// two ranges of query rows, swept in this order:
+//   X: response rows x_row0 .. x_row0 + x_len - 1 (Q_R, dO_R, LSE_R, D_R),
+//      causal if KV_X_CAUSAL, otherwise every key visible;
+//   Y: prompt rows y_row0 .. y_row0 + y_len - 1 (Q_P, ...), causal.
+// In a causal range, query i sits at position kpos0 + i of its segment (the
+// range starts at the tile's first key) and key j at kpos0 + j: visible iff
+// j <= i. Outputs: the key rows' dK/dV, in bf16 (KV_OUT_BF16) and/or into
+// fp32 slab `part` (KV_OUT_SLAB).
 struct KVTile {
   int32_t kv_row0, kv_len;
-  int32_t q_row0, q_len;
-  int32_t causal, kpos0, qpos0;
-  int32_t part;
+  int32_t x_row0, x_len;
+  int32_t y_row0, y_len;
+  int32_t kpos0;
+  int32_t flags;  // KV_* | part << KV_PART_SHIFT
+};
+
+enum : int32_t {
+  KV_PROMPT_KEYS = 1,  // keys K_P/V_P (outputs dK_P/dV_P); otherwise K_R/V_R
+  KV_X_CAUSAL = 2,
+  KV_OUT_BF16 = 4,
+  KV_OUT_SLAB = 8,
+  KV_PART_SHIFT = 8,
 };
 
 }  // namespace augtree

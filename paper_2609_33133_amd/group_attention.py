@@ -1,10 +1,13 @@
 """One pass of shared-prompt group attention, forward and backward, on the GPU,
 and the flattened per-branch baseline built from the same kernels.
 
-SharedStep (the method, §3.2-§3.3): prefill_fwd once per tree, replay_fwd of
-every branch against the stationary prompt KV plus its own causal KV,
-replay_bwd (branch gradients plus the prompt-KV seeds, Eq. 2), prefill_bwd
-(the prompt queries' own contribution), prompt_grad_reduce (self + seeds).
+SharedStep (the method, §3.2-§3.3): the prompt prefilled once per tree, every
+branch replayed against the stationary prompt KV plus its own causal KV, the
+branch gradients with every branch's prompt-KV gradient accumulated on the
+prompt KV (Eq. 2) together with the prompt queries' own contribution. By
+default as augtree_tree_fwd + augtree_tree_bwd; ``path="calls"`` strings the
+six separate entry points (prefill_fwd, replay_fwd, replay_bwd, prefill_bwd,
+prompt_grad_reduce).
 
 FlattenedStep (the baseline the paper compares against, §2.1): each branch as
 its own causal sequence [P; R_i]; the prompt is recomputed once per branch and
@@ -49,9 +52,18 @@ def default_n_seed(batch: GroupBatch, min_workgroups: int = 1024) -> int:
 
 
 class SharedStep:
-    def __init__(self, batch: GroupBatch, device="cuda", mode: int = REPLAY_FUSED, n_seed: Optional[int] = None):
+    """One step of the method on a fixed batch. ``path="tree"`` (default) runs
+    it as augtree_tree_fwd + augtree_tree_bwd (fewest launches; the Eq. 2 sum
+    in registers); ``path="calls"`` runs the six separate entry points
+    (prefill_fwd, replay_fwd, replay_bwd, prefill_bwd, prompt_grad_reduce)."""
+
+    def __init__(self, batch: GroupBatch, device="cuda", mode: int = REPLAY_FUSED, n_seed: Optional[int] = None,
+                 path: str = "tree"):
+        if path not in ("tree", "calls"):
+            raise ValueError(f"path {path!r}")
         self.b = b = batch
         self.mode = mode
+        self.path = path
         self.n_seed = default_n_seed(b) if n_seed is None else int(n_seed)
         dev = torch.device(device)
         f32, bf = torch.float32, torch.bfloat16
@@ -66,25 +78,58 @@ class SharedStep:
         self.dq_r = torch.empty((b.tr, b.hq, b.d), dtype=bf, device=dev)
         self.dk_r = torch.empty((b.tr, b.hkv, b.d), dtype=bf, device=dev)
         self.dv_r = torch.empty((b.tr, b.hkv, b.d), dtype=bf, device=dev)
-        self.seed = torch.empty((self.n_seed, 2, b.tp, b.hkv, b.d), dtype=f32, device=dev)
         self.dq_p = torch.empty((b.tp, b.hq, b.d), dtype=bf, device=dev)
-        self.dkv_self = torch.empty((2, b.tp, b.hkv, b.d), dtype=f32, device=dev)
         self.dkv_p = torch.empty((2, b.tp, b.hkv, b.d), dtype=bf, device=dev)
-        self.ws = {
-            "pf": b.workspace(api.OP_PREFILL_FWD, 0, dev),
-            "rf": b.workspace(api.OP_REPLAY_FWD, mode, dev),
-            "rb": b.workspace(api.OP_REPLAY_BWD, self.n_seed, dev),
-            "pb": b.workspace(api.OP_PREFILL_BWD, 0, dev),
-        }
+        if path == "calls":
+            self.seed = torch.empty((self.n_seed, 2, b.tp, b.hkv, b.d), dtype=f32, device=dev)
+            self.dkv_self = torch.empty((2, b.tp, b.hkv, b.d), dtype=f32, device=dev)
+            self.ws = {
+                "pf": b.workspace(api.OP_PREFILL_FWD, 0, dev),
+                "rf": b.workspace(api.OP_REPLAY_FWD, mode, dev),
+                "rb": b.workspace(api.OP_REPLAY_BWD, self.n_seed, dev),
+                "pb": b.workspace(api.OP_PREFILL_BWD, 0, dev),
+            }
+        else:
+            self.ws = {"tf": b.workspace(api.OP_TREE_FWD, mode, dev), "tb": b.workspace(api.OP_TREE_BWD, 0, dev)}
+        self._bound = None
+
+    def _bind(self, x: Dict[str, torch.Tensor]):
+        """ctypes argument tuples of the two tree calls for inputs ``x`` (the
+        pointers of every buffer are fixed), so a step is two foreign calls."""
+        b, P = self.b, api._ptr
+        for n in TENSORS:
+            rows = b.tp if n.endswith("_p") else b.tr
+            heads = b.hkv if n[0] in "kv" else b.hq
+            api._need(x[n], n, torch.bfloat16, (rows, heads, b.d))
+        fwd = [b.ref, self.mode, P(x["q_p"]), P(x["k_p"]), P(x["v_p"]), P(x["q_r"]), P(x["k_r"]), P(x["v_r"]),
+               P(self.o_p), P(self.lse_p), P(self.o_r), P(self.lse_r), P(self.o_part), P(self.lse_part),
+               P(self.ws["tf"]), self.ws["tf"].numel()]
+        bwd = [b.ref, P(x["q_p"]), P(x["k_p"]), P(x["v_p"]), P(self.o_p), P(self.lse_p), P(x["do_p"]),
+               P(x["q_r"]), P(x["k_r"]), P(x["v_r"]), P(self.o_r), P(self.lse_r), P(x["do_r"]),
+               P(self.dq_p), P(self.dkv_p[0]), P(self.dkv_p[1]), None, P(self.dq_r), P(self.dk_r), P(self.dv_r),
+               P(self.ws["tb"]), self.ws["tb"].numel()]
+        self._bound = (x, fwd, bwd)
 
     def forward(self, x: Dict[str, torch.Tensor], stream=None):
         b = self.b
+        if self.path == "tree":
+            if self._bound is None or self._bound[0] is not x:
+                self._bind(x)
+            lib = api._lib.load()
+            api._lib.check(lib.augtree_tree_fwd(*self._bound[1], api._stream(stream)), "tree_fwd")
+            return
         api.prefill_fwd(b, x["q_p"], x["k_p"], x["v_p"], self.o_p, self.lse_p, ws=self.ws["pf"], stream=stream)
         api.replay_fwd(b, x["q_r"], x["k_r"], x["v_r"], x["k_p"], x["v_p"], self.mode, self.o_r, self.lse_r,
                        self.o_part, self.lse_part, ws=self.ws["rf"], stream=stream)
 
     def backward(self, x: Dict[str, torch.Tensor], stream=None):
         b = self.b
+        if self.path == "tree":
+            if self._bound is None or self._bound[0] is not x:
+                self._bind(x)
+            lib = api._lib.load()
+            api._lib.check(lib.augtree_tree_bwd(*self._bound[2], api._stream(stream)), "tree_bwd")
+            return
         api.replay_bwd(b, x["q_r"], x["k_r"], x["v_r"], x["k_p"], x["v_p"], self.o_r, self.lse_r, x["do_r"],
                        self.n_seed, self.dq_r, self.dk_r, self.dv_r, self.seed, ws=self.ws["rb"], stream=stream)
         api.prefill_bwd(b, x["q_p"], x["k_p"], x["v_p"], self.o_p, self.lse_p, x["do_p"], self.dq_p, None,

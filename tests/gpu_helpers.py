@@ -28,9 +28,11 @@ def to_np(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
-def run_shared(gi, mode=REPLAY_FUSED, n_seed=None, device="cuda"):
+def run_shared(gi, mode=REPLAY_FUSED, n_seed=None, device="cuda", path="tree"):
+    """The method's step through the C ABI: path "tree" (augtree_tree_fwd +
+    augtree_tree_bwd) or "calls" (the six separate entry points)."""
     b = GroupBatch.from_shape(gi.shape)
-    step = SharedStep(b, device, mode=mode, n_seed=n_seed)
+    step = SharedStep(b, device, mode=mode, n_seed=n_seed, path=path)
     x = upload(gi, device)
     step.run(x)
     torch.cuda.synchronize()

@@ -25,8 +25,7 @@ def _write(path, rows):
 
 def test_kernel_names():
     n = bench.bench_kernel_name
-    assert n("void augtree::(anonymous namespace)::attn_dkv_kernel<128, true>(augtree::DkvParams)") == \
-        "attn_dkv_kernel<fp32 out>"
+    assert n("void augtree::(anonymous namespace)::attn_dkv_kernel<128>(augtree::DkvParams)") == "attn_dkv_kernel"
     assert n("void augtree::(anonymous namespace)::attn_fwd_kernel<64, false>(augtree::FwdParams)") == \
         "attn_fwd_kernel<bf16 out>"
     assert n("void augtree::(anonymous namespace)::attn_dq_kernel<128>(augtree::DqParams)") == "attn_dq_kernel"
@@ -35,7 +34,7 @@ def test_kernel_names():
 
 def test_pmc_summary_scales_by_copy_calibration(tmp_path):
     d = str(tmp_path)
-    k = "void augtree::(anonymous namespace)::attn_dkv_kernel<128, true>(augtree::DkvParams)"
+    k = "void augtree::(anonymous namespace)::attn_dkv_kernel<128>(augtree::DkvParams)"
     # copy of 1 GiB reads 2^19 KiB of FETCH_SIZE (factor 2) and 2^20 KiB of WRITE_SIZE (factor 1)
     _write(f"{d}/cfetch/run_counter_collection.csv", [(1, "copy", "FETCH_SIZE", 1 << 19)])
     _write(f"{d}/cwrite/run_counter_collection.csv", [(1, "copy", "WRITE_SIZE", 1 << 20)])
@@ -44,7 +43,7 @@ def test_pmc_summary_scales_by_copy_calibration(tmp_path):
     _write(f"{d}/write/run_counter_collection.csv", [(1, k, "WRITE_SIZE", 10.0), (2, k, "WRITE_SIZE", 30.0)])
     md = bench.summarize_pmc(d, "prompt")
     data = json.loads(re.search(r"<!-- traffic-json (\{.*\}) -->", md).group(1))
-    e = data["kernels"]["attn_dkv_kernel<fp32 out>"]
+    e = data["kernels"]["attn_dkv_kernel"]
     assert e["launches"] == 2
     assert e["fetch_bytes_per_launch"] == round(2000.0 * 1024 * 2)
     assert e["write_bytes_per_launch"] == round(20.0 * 1024)
@@ -99,3 +98,49 @@ def test_counter_summary_busy_and_bandwidth(tmp_path):
     wr("sq", [(1, k, "SQ_VALU_MFMA_BUSY_CYCLES", 25600.0, 0, 1000), (1, k, "GRBM_GUI_ACTIVE", 800.0, 0, 1000)])
     md = bench.summarize_counters(d)
     assert "| lse_merge_kernel | 1 | 0.001 | 25.0 | 2048 | 512 |" in md
+
+
+def test_pmc_summary_per_role(tmp_path):
+    """Library dispatches are attributed to the logged launch roles in order;
+    other kernels (runtime copies) are skipped; a count mismatch is an error."""
+    d = str(tmp_path)
+    fw = "void augtree::(anonymous namespace)::attn_fwd_kernel<128, false>(augtree::FwdParams)"
+    dq = "void augtree::(anonymous namespace)::attn_dq_kernel<128>(augtree::DqParams)"
+    _write(f"{d}/cfetch/run_counter_collection.csv", [(1, "copy", "FETCH_SIZE", 1 << 19)])
+    _write(f"{d}/cwrite/run_counter_collection.csv", [(1, "copy", "WRITE_SIZE", 1 << 20)])
+    rows_f = [(1, fw, "FETCH_SIZE", 100.0), (2, "copy", "FETCH_SIZE", 7.0), (3, fw, "FETCH_SIZE", 300.0),
+              (4, dq, "FETCH_SIZE", 50.0), (5, fw, "FETCH_SIZE", 900.0)]
+    rows_w = [(1, fw, "WRITE_SIZE", 10.0), (3, fw, "WRITE_SIZE", 30.0), (4, dq, "WRITE_SIZE", 5.0),
+              (5, fw, "WRITE_SIZE", 90.0)]
+    _write(f"{d}/fetch/run_counter_collection.csv", rows_f)
+    _write(f"{d}/write/run_counter_collection.csv", rows_w)
+    roles = tmp_path / "roles.json"
+    roles.write_text(json.dumps({"launches": ["shared:fwd_prefill", "shared:fwd_replay", "shared:dq_replay",
+                                              "flattened:fwd_prefill"], "flattened_rows": 100}))
+    md = bench.summarize_pmc(d, "tiny", str(roles))
+    data = json.loads(re.search(r"<!-- traffic-json (\{.*\}) -->", md).group(1))
+    r = data["roles"]
+    assert r["shared:fwd_replay"]["fetch_bytes_per_launch"] == round(300.0 * 1024 * 2)
+    assert r["flattened:fwd_prefill"]["write_bytes_per_launch"] == round(90.0 * 1024)
+    assert "shared:dq_replay" in md
+    roles.write_text(json.dumps({"launches": ["shared:fwd_prefill"]}))
+    try:
+        bench.summarize_pmc(d, "tiny", str(roles))
+        raise AssertionError("count mismatch not detected")
+    except ValueError:
+        pass
+
+
+def test_algorithmic_bytes_count_prompt_kv_once():
+    """The replay forward's minimum reads hold the prompt KV once; the
+    flattened forward's hold its private copies (G per group)."""
+    from paper_2609_33133_amd import inputs as I
+    s = I.config_shape("prompt")
+    rd, wr = bench.algorithmic_bytes("shared:fwd_replay", s)
+    kvp = 2 * s.total_prompt * s.num_kv_heads * s.head_dim * 2
+    q = s.total_resp * s.num_q_heads * s.head_dim * 2
+    assert rd == q + kvp + 2 * s.total_resp * s.num_kv_heads * s.head_dim * 2
+    assert wr == q + s.total_resp * s.num_q_heads * 4
+    flat_rows = 8 * 32768 + s.total_resp
+    rd_f, _ = bench.algorithmic_bytes("flattened:fwd_prefill", s, flat_rows)
+    assert rd_f > 7 * kvp

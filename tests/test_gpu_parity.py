@@ -25,12 +25,13 @@ def _device():
     assert lib.augtree_check_device() == 0, lib.augtree_last_error()
 
 
+@pytest.mark.parametrize("path", ["tree", "calls"])
 @pytest.mark.parametrize("mode", [REPLAY_FUSED, REPLAY_SPLIT])
-def test_tiny_workload_full_parity(mode):
+def test_tiny_workload_full_parity(mode, path):
     gi = I.make_config("tiny")
     ref = oracle(gi)
-    got, _ = run_shared(gi, mode=mode)
-    assert_close(got, ref, f"tiny mode={mode}")
+    got, _ = run_shared(gi, mode=mode, path=path)
+    assert_close(got, ref, f"tiny mode={mode} path={path}")
 
 
 SHAPES = [
@@ -57,9 +58,10 @@ def test_small_shapes(case):
     gi = I.make_inputs(shape, seed=100 + case, qk_mult=mult)
     log(f"case {case}: P={ps} R={rs} hq={hq} hkv={hkv} d={d} mult={mult}")
     ref = oracle(gi)
-    for mode in (REPLAY_FUSED, REPLAY_SPLIT):
-        got, _ = run_shared(gi, mode=mode)
-        assert_close(got, ref, f"case {case} mode {mode}")
+    for path in ("tree", "calls"):
+        for mode in (REPLAY_FUSED, REPLAY_SPLIT):
+            got, _ = run_shared(gi, mode=mode, path=path)
+            assert_close(got, ref, f"case {case} mode {mode} path {path}")
 
 
 @pytest.mark.parametrize("seed", [0, 1, 2, 3])
@@ -71,8 +73,10 @@ def test_random_ragged_shapes(seed):
     log(f"seed {seed}: P={shape.prompt_lens} R={shape.branch_lens} h={shape.num_q_heads}/{shape.num_kv_heads} "
         f"d={shape.head_dim}")
     ref = oracle(gi)
-    got, _ = run_shared(gi, n_seed=1 + seed)
-    assert_close(got, ref, f"random {seed}")
+    got, _ = run_shared(gi, n_seed=1 + seed, path="calls")
+    assert_close(got, ref, f"random {seed} calls n_seed={1 + seed}")
+    got, _ = run_shared(gi, mode=api.REPLAY_AUTO)
+    assert_close(got, ref, f"random {seed} tree auto")
 
 
 def test_q_zero_probe_closed_form():
@@ -87,8 +91,8 @@ def test_q_zero_probe_closed_form():
         for b in range(shape.cu_branch[g], shape.cu_branch[g + 1]):
             r0, r1 = shape.cu_resp[b], shape.cu_resp[b + 1]
             gi.v_r[r0:r1, :, 0] = I.f32_to_bf16_bits((p1 - p0 + np.arange(r1 - r0)).astype(np.float32))[:, None]
-    for mode in (REPLAY_FUSED, REPLAY_SPLIT):
-        got, _ = run_shared(gi, mode=mode)
+    for mode, path in ((REPLAY_FUSED, "tree"), (REPLAY_SPLIT, "tree"), (REPLAY_FUSED, "calls")):
+        got, _ = run_shared(gi, mode=mode, path=path)
         for g in range(shape.num_groups):
             p0, p1 = shape.cu_prompt[g], shape.cu_prompt[g + 1]
             P = p1 - p0
@@ -125,9 +129,9 @@ def test_rising_logits_move_the_softmax_reference():
         pos = (P + np.arange(r1 - r0, dtype=np.float32)) / 640
         gi.k_r[r0:r1, :, 0] = I.f32_to_bf16_bits(pos[:, None].repeat(2, 1))
     ref = oracle(gi)
-    for mode in (REPLAY_FUSED, REPLAY_SPLIT):
-        got, _ = run_shared(gi, mode=mode)
-        assert_close(got, ref, f"rising logits mode {mode}")
+    for mode, path in ((REPLAY_FUSED, "tree"), (REPLAY_SPLIT, "tree"), (REPLAY_FUSED, "calls")):
+        got, _ = run_shared(gi, mode=mode, path=path)
+        assert_close(got, ref, f"rising logits mode {mode} path {path}")
 
 
 def test_fused_equals_split():
@@ -141,14 +145,15 @@ def test_fused_equals_split():
         assert rel(a[k], b[k]) < 5e-3, k
 
 
-def test_determinism_bitwise():
+@pytest.mark.parametrize("path", ["tree", "calls"])
+def test_determinism_bitwise(path):
     shape = I.custom_shape([300, 90], [[100, 200, 5], [65, 129]], 8, 2, 128)
     gi = I.make_inputs(shape, seed=9)
     b = GroupBatch.from_shape(shape)
     x = upload(gi)
     outs = []
     for _ in range(3):
-        step = SharedStep(b, "cuda", n_seed=3)
+        step = SharedStep(b, "cuda", n_seed=3, path=path)
         step.run(x)
         torch.cuda.synchronize()
         outs.append({k: v.clone() for k, v in step.outputs().items()})
@@ -172,9 +177,9 @@ def _batch_of(parts):
     return I.GroupInputs(shape=shape, **fields)
 
 
-def _run_step(gi, prefill_bwd_first=False):
+def _run_step(gi, prefill_bwd_first=False, path="calls"):
     b = GroupBatch.from_shape(gi.shape)
-    step = SharedStep(b, "cuda", mode=REPLAY_FUSED, n_seed=2)
+    step = SharedStep(b, "cuda", mode=REPLAY_FUSED, n_seed=2, path=path)
     x = upload(gi)
     step.forward(x)
     if prefill_bwd_first:
@@ -204,12 +209,20 @@ def test_outputs_independent_of_batch_and_call_order():
     tp_a, tr_a, tp_b, tr_b = 300, 305, 90, 194
     for parts, p0, r0 in (([a, b], 0, 0), ([b, a], tp_b, tr_b)):
         got = _run_step(_batch_of(parts))
-        rows = {"o_p": (p0, tp_a), "dq_p": (p0, tp_a), "dk_p": (p0, tp_a), "dv_p": (p0, tp_a),
-                "o_r": (r0, tr_a), "dq_r": (r0, tr_a), "dk_r": (r0, tr_a), "dv_r": (r0, tr_a)}
-        for k, (o, n) in rows.items():
-            assert torch.equal(_bits(got[k][o:o + n]), _bits(alone[k])), f"batch position {p0}: {k}"
-        assert torch.equal(_bits(got["lse_p"][:, p0:p0 + tp_a]), _bits(alone["lse_p"])), "lse_p"
-        assert torch.equal(_bits(got["lse_r"][:, r0:r0 + tr_a]), _bits(alone["lse_r"])), "lse_r"
+        _same_rows(got, alone, p0, r0, tp_a, tr_a)
+    alone = _run_step(a, path="tree")
+    for parts, p0, r0 in (([a, b], 0, 0), ([b, a], tp_b, tr_b)):
+        _same_rows(_run_step(_batch_of(parts), path="tree"), alone, p0, r0, tp_a, tr_a)
+
+
+def _same_rows(got, alone, p0, r0, tp_a, tr_a):
+    """The rows of tree `a` inside a batch output are bitwise its outputs alone."""
+    rows = {"o_p": (p0, tp_a), "dq_p": (p0, tp_a), "dk_p": (p0, tp_a), "dv_p": (p0, tp_a),
+            "o_r": (r0, tr_a), "dq_r": (r0, tr_a), "dk_r": (r0, tr_a), "dv_r": (r0, tr_a)}
+    for k, (o, n) in rows.items():
+        assert torch.equal(_bits(got[k][o:o + n]), _bits(alone[k])), f"batch position {p0}: {k}"
+    assert torch.equal(_bits(got["lse_p"][:, p0:p0 + tp_a]), _bits(alone["lse_p"])), "lse_p"
+    assert torch.equal(_bits(got["lse_r"][:, r0:r0 + tr_a]), _bits(alone["lse_r"])), "lse_r"
 
 
 @pytest.mark.parametrize("n_seed", [1, 2, 5])
@@ -217,7 +230,7 @@ def test_seed_chunks_give_same_prompt_gradient(n_seed):
     shape = I.custom_shape([200], [[150, 150, 40, 300]], 8, 2, 128)
     gi = I.make_inputs(shape, seed=10)
     ref = oracle(gi)
-    got, step = run_shared(gi, n_seed=n_seed)
+    got, step = run_shared(gi, n_seed=n_seed, path="calls")
     assert_close(got, ref, f"n_seed={n_seed}")
     # every slab holds its chunk's contribution; their sum is the branch total
     sh = A.shared_fwd_bwd(shape.cu_prompt, shape.cu_branch, shape.cu_resp, 8, 2, shape.scale,
@@ -313,8 +326,9 @@ def test_auto_mode_mixed_groups():
     assert api.replay_split_groups(b).tolist() == [1, 0, 1]
     gi = I.make_inputs(shape, seed=41, qk_mult=1.0)
     ref = oracle(gi)
-    got, _ = run_shared(gi, mode=api.REPLAY_AUTO)
-    assert_close(got, ref, "auto mixed")
+    for path in ("tree", "calls"):
+        got, _ = run_shared(gi, mode=api.REPLAY_AUTO, path=path)
+        assert_close(got, ref, f"auto mixed {path}")
 
 
 @pytest.mark.parametrize("ps,rs,same_as", [([300], [[250, 260]], REPLAY_FUSED), ([1000], [[3] * 20], REPLAY_SPLIT)])
