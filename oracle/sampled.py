@@ -20,6 +20,13 @@ import numpy as np
 _BLOCK = 256
 
 
+def _block_rows(n_keys: int) -> int:
+    """Query rows per block against ``n_keys`` keys: at most 2^21 scores (16 MB
+    of float64 per temporary), so the temporaries of one block are reused from
+    the heap instead of being mapped and faulted in afresh for every block."""
+    return int(max(16, min(_BLOCK, (1 << 21) // max(n_keys, 1))))
+
+
 def _f64(bits: np.ndarray) -> np.ndarray:
     """bf16 bit patterns -> float64 (exact)."""
     return (np.asarray(bits, dtype=np.uint16).astype(np.uint32) << np.uint32(16)).view(np.float32).astype(np.float64)
@@ -93,7 +100,77 @@ def query_rows(t, kind: str, rows: Sequence[int], head: int) -> Dict[str, np.nda
     return {"o": o, "lse": lse, "dq": dq}
 
 
-def key_rows(t, kind: str, rows: Sequence[int], kv_head: int) -> Dict[str, np.ndarray]:
+def _key_unit(t, kind, cols, kv_head, h, seg):
+    """dK, dV of the key columns ``cols`` (positions inside the key set of
+    ``seg``) from the queries of one query head ``h`` in one range of query
+    rows: seg = ("prefill", g, a0, a1) the prompt rows a0 .. a1-1 of group g
+    (keys = that prompt, causal), ("branch", b, a0, a1) the rows a0 .. a1-1 of
+    branch b (keys = its group's prompt followed by its own prefix). For kind
+    "resp" the columns are positions inside branch b's own keys."""
+    scale = 1.0 / np.sqrt(t.head_dim)
+    d = t.head_dim
+    cols = np.asarray(cols)
+    dk = np.zeros((len(cols), d))
+    dv = np.zeros((len(cols), d))
+    a0, a1 = seg[2], seg[3]
+    if seg[0] == "prefill":
+        g = seg[1]
+        p0, p1 = int(t.cu_prompt[g]), int(t.cu_prompt[g + 1])
+        P = p1 - p0
+        kp, vp = _keyset_prompt(t, g, kv_head, P)
+        step = _block_rows(P)
+        for a in range(a0, a1, step):
+            bnd = min(a1, a + step)
+            q = _f64(t.q_p[p0 + a:p0 + bnd, h])
+            do = _f64(t.do_p[p0 + a:p0 + bnd, h])
+            vis = np.arange(bnd)[None, :] <= np.arange(a, bnd)[:, None]
+            _, _, p, ds = _rows_block(q, do, kp[:bnd], vp[:bnd], vis, scale)
+            sel = cols < bnd
+            dk[sel] += scale * (ds[:, cols[sel]].T @ q)
+            dv[sel] += p[:, cols[sel]].T @ do
+        return dk, dv
+    b = seg[1]
+    g = _group_of_branch(t.cu_branch, b)
+    r0, r1 = int(t.cu_resp[b]), int(t.cu_resp[b + 1])
+    P = int(t.cu_prompt[g + 1] - t.cu_prompt[g])
+    kp, vp = _keyset_prompt(t, g, kv_head, P)
+    kr, vr = _f64(t.k_r[r0:r1, kv_head]), _f64(t.v_r[r0:r1, kv_head])
+    kk, vv = np.concatenate([kp, kr]), np.concatenate([vp, vr])
+    c = cols if kind == "prompt" else cols + P
+    step = _block_rows(P + r1 - r0)
+    for a in range(a0, a1, step):
+        bnd = min(a1, a + step)
+        q = _f64(t.q_r[r0 + a:r0 + bnd, h])
+        do = _f64(t.do_r[r0 + a:r0 + bnd, h])
+        vis = np.concatenate([np.ones((bnd - a, P), dtype=bool),
+                              np.arange(r1 - r0)[None, :] <= np.arange(a, bnd)[:, None]], axis=1)
+        _, _, p, ds = _rows_block(q, do, kk, vv, vis, scale)
+        sel = np.ones(len(cols), dtype=bool) if kind == "prompt" else cols < bnd
+        dk[sel] += scale * (ds[:, c[sel]].T @ q)
+        dv[sel] += p[:, c[sel]].T @ do
+    return dk, dv
+
+
+# query rows per term of key_rows (terms are computed independently and
+# added in order)
+_TERM_ROWS = 2048
+
+
+def _ranges(a0, a1):
+    return [(a, min(a1, a + _TERM_ROWS)) for a in range(a0, a1, _TERM_ROWS)]
+
+
+_UNIT_ARGS = None
+
+
+def _key_unit_idx(i):
+    # one BLAS thread per worker process: the pool supplies the parallelism
+    from threadpoolctl import threadpool_limits
+    with threadpool_limits(1):
+        return _key_unit(*_UNIT_ARGS[i])
+
+
+def key_rows(t, kind: str, rows: Sequence[int], kv_head: int, workers: int = 1) -> Dict[str, np.ndarray]:
     """dK and dV of packed key rows ``rows`` of KV head ``kv_head``, summed over
     the query heads of that KV head and over every query that sees the key.
 
@@ -102,67 +179,50 @@ def key_rows(t, kind: str, rows: Sequence[int], kv_head: int) -> Dict[str, np.nd
     response row of the group (this is the total of Eq. 2: the prefill
     contribution plus every branch's contribution). kind "resp": all rows must
     belong to one branch; the queries are that branch's rows at or after the
-    earliest sampled key."""
-    scale = 1.0 / np.sqrt(t.head_dim)
+    earliest sampled key.
+
+    The sum runs over (query head, range of query rows) terms in a fixed
+    order: for each query head, the prompt rows first, then the branches in
+    index order (Eq. 2's order), each in ranges of _TERM_ROWS rows. ``workers``
+    > 1 computes the terms in a process pool and adds them in the same order,
+    so the result is the same bit for bit."""
     gq = t.num_q_heads // t.num_kv_heads
     rows = [int(r) for r in rows]
     d = t.head_dim
-    dk = np.zeros((len(rows), d))
-    dv = np.zeros((len(rows), d))
+    units = []
     if kind == "prompt":
         g = _group_of_prompt_row(t.cu_prompt, rows[0])
         p0, p1 = int(t.cu_prompt[g]), int(t.cu_prompt[g + 1])
         assert all(p0 <= r < p1 for r in rows)
         cols = np.array([r - p0 for r in rows])
-        P = p1 - p0
-        kp, vp = _keyset_prompt(t, g, kv_head, P)
-        first = int(cols.min())
         for h in range(kv_head * gq, kv_head * gq + gq):
-            # prefill queries at positions >= first
-            for a in range(first, P, _BLOCK):
-                bnd = min(P, a + _BLOCK)
-                q = _f64(t.q_p[p0 + a:p0 + bnd, h])
-                do = _f64(t.do_p[p0 + a:p0 + bnd, h])
-                vis = np.arange(bnd)[None, :] <= np.arange(a, bnd)[:, None]
-                _, _, p, ds = _rows_block(q, do, kp[:bnd], vp[:bnd], vis, scale)
-                sel = cols < bnd
-                dk[sel] += scale * (ds[:, cols[sel]].T @ q)
-                dv[sel] += p[:, cols[sel]].T @ do
-            # every response row of every branch of the group
+            for a, z in _ranges(int(cols.min()), p1 - p0):
+                units.append((t, kind, cols, kv_head, h, ("prefill", g, a, z)))
             for b in range(int(t.cu_branch[g]), int(t.cu_branch[g + 1])):
-                r0, r1 = int(t.cu_resp[b]), int(t.cu_resp[b + 1])
-                kr, vr = _f64(t.k_r[r0:r1, kv_head]), _f64(t.v_r[r0:r1, kv_head])
-                kk, vv = np.concatenate([kp, kr]), np.concatenate([vp, vr])
-                for a in range(0, r1 - r0, _BLOCK):
-                    bnd = min(r1 - r0, a + _BLOCK)
-                    q = _f64(t.q_r[r0 + a:r0 + bnd, h])
-                    do = _f64(t.do_r[r0 + a:r0 + bnd, h])
-                    vis = np.concatenate([np.ones((bnd - a, P), dtype=bool),
-                                          np.arange(r1 - r0)[None, :] <= np.arange(a, bnd)[:, None]], axis=1)
-                    _, _, p, ds = _rows_block(q, do, kk, vv, vis, scale)
-                    dk += scale * (ds[:, cols].T @ q)
-                    dv += p[:, cols].T @ do
+                for a, z in _ranges(0, int(t.cu_resp[b + 1] - t.cu_resp[b])):
+                    units.append((t, kind, cols, kv_head, h, ("branch", b, a, z)))
     else:
         b = _branch_of_resp_row(t.cu_resp, rows[0])
         r0, r1 = int(t.cu_resp[b]), int(t.cu_resp[b + 1])
         assert all(r0 <= r < r1 for r in rows)
-        g = _group_of_branch(t.cu_branch, b)
-        P = int(t.cu_prompt[g + 1] - t.cu_prompt[g])
         cols = np.array([r - r0 for r in rows])
-        kp, vp = _keyset_prompt(t, g, kv_head, P)
-        kr, vr = _f64(t.k_r[r0:r1, kv_head]), _f64(t.v_r[r0:r1, kv_head])
-        kk, vv = np.concatenate([kp, kr]), np.concatenate([vp, vr])
-        first = int(cols.min())
         for h in range(kv_head * gq, kv_head * gq + gq):
-            for a in range(first, r1 - r0, _BLOCK):
-                bnd = min(r1 - r0, a + _BLOCK)
-                q = _f64(t.q_r[r0 + a:r0 + bnd, h])
-                do = _f64(t.do_r[r0 + a:r0 + bnd, h])
-                vis = np.concatenate([np.ones((bnd - a, P), dtype=bool),
-                                      np.arange(r1 - r0)[None, :] <= np.arange(a, bnd)[:, None]], axis=1)
-                _, _, p, ds = _rows_block(q, do, kk, vv, vis, scale)
-                c = cols + P
-                sel = cols < bnd
-                dk[sel] += scale * (ds[:, c[sel]].T @ q)
-                dv[sel] += p[:, c[sel]].T @ do
+            for a, z in _ranges(int(cols.min()), r1 - r0):
+                units.append((t, kind, cols, kv_head, h, ("branch", b, a, z)))
+    if workers > 1 and len(units) > 1:
+        import multiprocessing as mp
+        global _UNIT_ARGS
+        _UNIT_ARGS = units
+        try:
+            with mp.get_context("fork").Pool(min(workers, len(units))) as pool:
+                parts = pool.map(_key_unit_idx, range(len(units)), chunksize=1)
+        finally:
+            _UNIT_ARGS = None
+    else:
+        parts = [_key_unit(*u) for u in units]
+    dk = np.zeros((len(rows), d))
+    dv = np.zeros((len(rows), d))
+    for a, b in parts:
+        dk = dk + a
+        dv = dv + b
     return {"dk": dk, "dv": dv}

@@ -358,6 +358,25 @@ def test_sampled_rows_match_flattened():
             assert rel(got["dv"], fl["dv_r"][rows, kh]) < 1e-12
 
 
+def test_sampled_key_rows_pool_matches_serial():
+    """The pooled key-row reference adds the same terms in the same order as
+    the serial one: identical bits."""
+    s = SMALL
+    gi = I.make_inputs(s, seed=20, qk_mult=1.0)
+
+    class T:
+        pass
+    t = T()
+    t.cu_prompt, t.cu_branch, t.cu_resp = s.cu_prompt, s.cu_branch, s.cu_resp
+    t.num_q_heads, t.num_kv_heads, t.head_dim = 4, 2, 16
+    for name in ("q_p", "k_p", "v_p", "q_r", "k_r", "v_r", "do_p", "do_r"):
+        setattr(t, name, getattr(gi, name))
+    for kind, rows in (("prompt", [0, 4, 12]), ("prompt", [13, 17, 18]), ("resp", [12, 13, 15])):
+        a = S.key_rows(t, kind, rows, 1)
+        b = S.key_rows(t, kind, rows, 1, workers=3)
+        assert np.array_equal(a["dk"], b["dk"]) and np.array_equal(a["dv"], b["dv"])
+
+
 # --------------------------------------------------------------------------- golden regression
 
 def test_golden_tiny_fixture():
