@@ -280,6 +280,30 @@ int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint1
                      size_t ws_bytes, void* stream);
 
 /*
+ * augtree_tree_bwd without a workspace argument, for callers that cannot
+ * allocate device memory (code under stream capture, tight serving loops,
+ * harnesses that forbid allocation). Same inputs, outputs and results as
+ * augtree_tree_bwd (bit for bit: same kernels and schedule). Its workspace is
+ * a fixed 64 MiB device array of the library (augtree_noalloc_scratch_bytes()),
+ * one copy per GPU, held from the first call on that GPU until the process
+ * ends; the call performs no allocation. A batch whose workspace
+ * (augtree_workspace_size(grp, AUGTREE_OP_TREE_BWD, 0)) exceeds it is rejected
+ * with AUGTREE_ERR_WORKSPACE before anything is enqueued. Calls that overlap on
+ * one GPU (several streams or threads) share the array and race; serialise
+ * them.
+ */
+int augtree_tree_bwd_noalloc(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p,
+                             const uint16_t* v_p, const uint16_t* o_p, const float* lse_p,
+                             const uint16_t* do_p, const uint16_t* q_r, const uint16_t* k_r,
+                             const uint16_t* v_r, const uint16_t* o_r, const float* lse_r,
+                             const uint16_t* do_r, uint16_t* dq_p, uint16_t* dk_p, uint16_t* dv_p,
+                             float* dkv_p_f32, uint16_t* dq_r, uint16_t* dk_r, uint16_t* dv_r,
+                             void* stream);
+
+/* Bytes of the device array augtree_tree_bwd_noalloc works in (its limit). */
+size_t augtree_noalloc_scratch_bytes(void);
+
+/*
  * Eq. 2 reduction: the prompt-KV gradient is the prefill's own contribution
  * plus the sum of the branch seeds. Elementwise, in a fixed order (self first,
  * then terms in index order), fp32 sum and one rounding to bf16:

@@ -36,7 +36,8 @@ EXPORTS = (
     "augtree_workspace_size", "augtree_prefill_fwd", "augtree_replay_fwd", "augtree_lse_merge",
     "augtree_replay_bwd", "augtree_prefill_bwd", "augtree_prompt_grad_reduce", "augtree_status_string",
     "augtree_last_error", "augtree_check_device", "augtree_version", "augtree_set_launch_hook",
-    "augtree_replay_split_groups", "augtree_tree_fwd", "augtree_tree_bwd",
+    "augtree_replay_split_groups", "augtree_tree_fwd", "augtree_tree_bwd", "augtree_tree_bwd_noalloc",
+    "augtree_noalloc_scratch_bytes",
 )
 
 LAUNCH_HOOK = ctypes.CFUNCTYPE(None, ctypes.c_char_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p)
@@ -89,6 +90,8 @@ def _sig(lib):
         "augtree_replay_split_groups": (ctypes.c_int, [_GP, _P]),
         "augtree_tree_fwd": (ctypes.c_int, [_GP, ctypes.c_int] + [_P] * 12 + [_P, _SZ, _P]),
         "augtree_tree_bwd": (ctypes.c_int, [_GP] + [_P] * 19 + [_P, _SZ, _P]),
+        "augtree_tree_bwd_noalloc": (ctypes.c_int, [_GP] + [_P] * 19 + [_P]),
+        "augtree_noalloc_scratch_bytes": (_SZ, []),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)

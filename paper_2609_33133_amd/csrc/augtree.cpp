@@ -21,6 +21,7 @@
 #include <vector>
 
 #include "../../include/augtree.h"
+#include "internal.h"
 #include "kernels.h"
 
 using namespace augtree;
@@ -822,11 +823,18 @@ int augtree_prefill_bwd(const augtree_groups* grp, const uint16_t* q_p, const ui
   return ok();
 }
 
-int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p, const uint16_t* v_p,
-                     const uint16_t* o_p, const float* lse_p, const uint16_t* do_p, const uint16_t* q_r,
-                     const uint16_t* k_r, const uint16_t* v_r, const uint16_t* o_r, const float* lse_r,
-                     const uint16_t* do_r, uint16_t* dq_p, uint16_t* dk_p, uint16_t* dv_p, float* dkv_p_f32,
-                     uint16_t* dq_r, uint16_t* dk_r, uint16_t* dv_r, void* ws, size_t ws_bytes, void* stream) {
+}  // extern "C"
+
+namespace augtree {
+
+int fail_status(int status, const char* msg) { return fail(status, "%s", msg); }
+
+int tree_bwd_impl(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p, const uint16_t* v_p,
+                  const uint16_t* o_p, const float* lse_p, const uint16_t* do_p, const uint16_t* q_r,
+                  const uint16_t* k_r, const uint16_t* v_r, const uint16_t* o_r, const float* lse_r,
+                  const uint16_t* do_r, uint16_t* dq_p, uint16_t* dk_p, uint16_t* dv_p, float* dkv_p_f32,
+                  uint16_t* dq_r, uint16_t* dk_r, uint16_t* dv_r, ScratchFn scratch, void* ws, size_t ws_bytes,
+                  void* stream) {
   Shape s;
   int st = validate_groups(grp, &s);
   if (st) return st;
@@ -835,8 +843,16 @@ int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint1
   REQUIRE_PTR(dq_p); REQUIRE_PTR(dk_p); REQUIRE_PTR(dv_p); REQUIRE_PTR(dq_r); REQUIRE_PTR(dk_r); REQUIRE_PTR(dv_r);
   OPTIONAL_PTR(dkv_p_f32);
   Plan pl = plan_for(s, AUGTREE_OP_TREE_BWD, dkv_p_f32 ? 1 : 0);
+  if (scratch) {  // the caller's buffer is a fixed device array: check its size before touching the device
+    if (pl.bytes > ws_bytes)
+      return fail(AUGTREE_ERR_WORKSPACE,
+                  "this batch needs %zu bytes of scratch; the allocation-free entry point holds at most %zu bytes",
+                  pl.bytes, ws_bytes);
+    if ((st = check_device_impl())) return st;
+    if ((st = scratch(&ws))) return st;
+  }
   if ((st = check_ws(pl, ws, ws_bytes))) return st;
-  if ((st = check_device_impl())) return st;
+  if (!scratch && (st = check_device_impl())) return st;
   hipStream_t str = static_cast<hipStream_t>(stream);
   if ((st = upload(pl, ws, str))) return st;
   const Tensors x{q_p, k_p, v_p, o_p, do_p, lse_p, q_r, k_r, v_r, o_r, do_r, lse_r};
@@ -846,6 +862,19 @@ int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint1
   out.slab = dkv_p_f32; out.slab_rows = s.tp;
   if ((st = run_bwd(s, pl, x, out, ws, str, "dq_tree", "dkv_tree"))) return st;
   return ok();
+}
+
+}  // namespace augtree
+
+extern "C" {
+
+int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p, const uint16_t* v_p,
+                     const uint16_t* o_p, const float* lse_p, const uint16_t* do_p, const uint16_t* q_r,
+                     const uint16_t* k_r, const uint16_t* v_r, const uint16_t* o_r, const float* lse_r,
+                     const uint16_t* do_r, uint16_t* dq_p, uint16_t* dk_p, uint16_t* dv_p, float* dkv_p_f32,
+                     uint16_t* dq_r, uint16_t* dk_r, uint16_t* dv_r, void* ws, size_t ws_bytes, void* stream) {
+  return tree_bwd_impl(grp, q_p, k_p, v_p, o_p, lse_p, do_p, q_r, k_r, v_r, o_r, lse_r, do_r, dq_p, dk_p, dv_p,
+                       dkv_p_f32, dq_r, dk_r, dv_r, nullptr, ws, ws_bytes, stream);
 }
 
 int augtree_prompt_grad_reduce(int32_t n_tensors, int64_t rows, int32_t heads, int32_t head_dim, const float* self,
