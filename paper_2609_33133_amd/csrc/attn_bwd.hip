@@ -28,8 +28,8 @@ namespace {
 
 // ----------------------------------------------------------------------------- dQ
 
-constexpr int DQ_BM = 128;
-constexpr int DQ_BN = 64;
+constexpr int DQ_BM = kDqBlockM;
+constexpr int DQ_BN = kDqBlockN;
 constexpr int DQ_DEPTH = 4;  // LDS operand reads run this many MFMAs ahead
 
 template <int D>
@@ -252,8 +252,8 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 
 // ----------------------------------------------------------------------------- dK/dV
 
-constexpr int KV_BN = 128;  // keys per workgroup (32 per wavefront pair)
-constexpr int KV_BQ = 64;   // query rows per block (32 per wavefront of a pair)
+constexpr int KV_BN = kDkvBlockN;  // keys per workgroup (32 per wavefront pair)
+constexpr int KV_BQ = kDkvBlockQ;  // query rows per block (32 per wavefront of a pair)
 constexpr int DKV_SDP_DEPTH = 3;  // LDS operand reads of S / dP run this many MFMAs ahead
 constexpr int DKV_DVK_DEPTH = 2;  // the same for the dV / dK transpose reads
 
@@ -519,9 +519,5 @@ hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, hipStream_t stream) 
   else hipLaunchKernelGGL((attn_dkv_kernel<64>), grid, block, 0, stream, p);
   return hipGetLastError();
 }
-
-int dq_block_m() { return DQ_BM; }
-int dkv_block_n() { return KV_BN; }
-int dkv_block_q() { return KV_BQ; }
 
 }  // namespace augtree

@@ -30,8 +30,8 @@ namespace augtree {
 
 namespace {
 
-constexpr int BM = 128;  // query rows per workgroup
-constexpr int BN = 64;   // keys per block
+constexpr int BM = kFwdBlockM;  // query rows per workgroup
+constexpr int BN = kFwdBlockN;  // keys per block
 constexpr int FWD_DEPTH = 4;  // LDS operand reads run this many MFMAs ahead
 constexpr int PV_DEPTH = 3;   // the same for the P V MFMAs (two reads each)
 constexpr int FWD_VALU_PER_MFMA = 7;  // softmax instructions placed after each S MFMA
@@ -278,8 +278,5 @@ hipError_t launch_attn_fwd(const FwdParams& p0, int n_tiles, bool out_f32, hipSt
   }
   return hipGetLastError();
 }
-
-int fwd_block_m() { return BM; }
-int fwd_block_n() { return BN; }
 
 }  // namespace augtree

@@ -83,10 +83,10 @@ hipError_t launch_grad_reduce(int n_tensors, int64_t rows, int64_t row_elems, co
                               int64_t part_rows, int64_t part_stride, const float* parts, const int32_t* row_map, uint16_t* out,
                               float* out32, hipStream_t stream);
 
-int fwd_block_m();
-int fwd_block_n();
-int dq_block_m();
-int dkv_block_n();
-int dkv_block_q();
+inline int fwd_block_m() { return kFwdBlockM; }
+inline int fwd_block_n() { return kFwdBlockN; }
+inline int dq_block_m() { return kDqBlockM; }
+inline int dkv_block_n() { return kDkvBlockN; }
+inline int dkv_block_q() { return kDkvBlockQ; }
 
 }  // namespace augtree

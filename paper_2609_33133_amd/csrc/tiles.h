@@ -8,6 +8,14 @@ namespace augtree {
 constexpr float kLog2e = 1.4426950408889634f;
 constexpr float kLn2 = 0.6931471805599453f;
 
+// Tile sizes of the kernels (the host schedules are cut to them).
+constexpr int kFwdBlockM = 128;   // forward: query rows per tile
+constexpr int kFwdBlockN = 64;    // forward: keys per block
+constexpr int kDqBlockM = 128;    // dQ: query rows per tile
+constexpr int kDqBlockN = 64;     // dQ: keys per block
+constexpr int kDkvBlockN = 128;   // dK/dV: keys per tile
+constexpr int kDkvBlockQ = 64;    // dK/dV: query rows per block
+
 // Query tile of the forward and dQ kernels: up to BM query rows, attending to
 // segment A (prompt keys, every key visible) and then segment B (causal:
 // query i of the tile sits at segment position b_qpos + i and sees keys

@@ -152,3 +152,23 @@ def test_valid_call_without_gpu_reports_device(L):
     need = L.augtree_workspace_size(ctypes.byref(g), 0, 0)
     assert L.augtree_prefill_fwd(ctypes.byref(g), p, p, p, p, p, p, need, None) == 5
     assert L.augtree_check_device() == 5
+
+
+def test_tree_calls_validate_on_the_host(L):
+    """The two tree calls reject bad arguments before any launch (statuses as
+    for the six calls), and the allocation-free backward rejects a batch whose
+    workspace exceeds its fixed device array before touching the device."""
+    g = groups(*GOOD)
+    p = fake()
+    need_f = L.augtree_workspace_size(ctypes.byref(g), 4, 0)
+    need_b = L.augtree_workspace_size(ctypes.byref(g), 5, 0)
+    assert need_f > 0 and need_b > 0 and need_b % 256 == 0
+    assert L.augtree_workspace_size(ctypes.byref(g), 4, 9) == 0          # unknown replay mode
+    assert L.augtree_tree_fwd(ctypes.byref(g), 1, *([p] * 6), *([p] * 4), None, None, p, need_f, None) == 1
+    assert L.augtree_tree_bwd(ctypes.byref(g), *([p] * 15), None, p, p, None, p, need_b, None) == 1   # null dv_r
+    assert L.augtree_tree_bwd(ctypes.byref(g), *([p] * 15), None, p, p, p, p, need_b - 1, None) == 4
+    assert L.augtree_noalloc_scratch_bytes() == 64 << 20
+    big = groups([0, 1 << 19], [0, 1], [0, 1 << 19], hq=32, hkv=8, d=128)
+    assert L.augtree_workspace_size(ctypes.byref(big), 5, 0) > (64 << 20)
+    st = L.augtree_tree_bwd_noalloc(ctypes.byref(big), *([p] * 15), None, p, p, p, None)
+    assert st == 4 and "allocation-free" in L.augtree_last_error().decode()
