@@ -209,13 +209,15 @@ def summarize_pmc(d: str, workload: str, roles_file: str = None) -> str:
             raise ValueError(f"{sub}: {len(lib_rows)} library dispatches but {len(roles['launches'])} logged launches")
         for i, (name, v) in enumerate(lib_rows):
             k = bench_kernel_name(name)
-            e = per.setdefault(k, {"fetch": [], "write": []})
-            e[key].append(v * 1024.0 * scale)
-            if roles is not None:
-                r = roles["launches"][i]
+            r = None if roles is None else roles["launches"][i]
+            if r is not None:
                 if ROLE_KERNEL[r.split(":", 1)[-1]] != k:
                     raise ValueError(f"dispatch {i}: kernel {k} but logged role {r}")
                 per_role.setdefault(r, {"fetch": [], "write": []})[key].append(v * 1024.0 * scale)
+            # the per-kernel figures (the bench line's roofline traffic) cover
+            # the shared step only, not the flattened baseline's launches
+            if r is None or r.startswith("shared:"):
+                per.setdefault(k, {"fetch": [], "write": []})[key].append(v * 1024.0 * scale)
 
     def avg(e):
         n = len(e["fetch"])
@@ -226,12 +228,14 @@ def summarize_pmc(d: str, workload: str, roles_file: str = None) -> str:
     kernels = {k: avg(e) for k, e in per.items()}
     roles_out = {r: avg(e) for r, e in per_role.items()}
     data = {"workload": workload, "source_hash": kernel_source_hash(),
+            "path": None if roles is None else roles.get("path"),
             "calibration": {"copy_bytes": copy_bytes, "copy_fetch_kib": cf, "copy_write_kib": cw,
                             "fetch_scale": round(f_scale, 4), "write_scale": round(w_scale, 4)},
             "kernels": kernels}
     if roles is not None:
         data["roles"] = roles_out
-    lines = ["| kernel | launches | HBM read GB / launch | HBM write GB / launch |", "|---|---|---|---|"]
+    lines = [("Shared step only (" + str(data["path"]) + " path):" if roles is not None else "Every library dispatch:"),
+             "", "| kernel | launches | HBM read GB / launch | HBM write GB / launch |", "|---|---|---|---|"]
     for k, v in sorted(kernels.items(), key=lambda kv: -kv[1]["bytes_per_launch"]):
         lines.append(f"| {k} | {v['launches']} | {v['fetch_bytes_per_launch'] / 1e9:.3f} | "
                      f"{v['write_bytes_per_launch'] / 1e9:.3f} |")
@@ -254,11 +258,13 @@ def summarize_pmc(d: str, workload: str, roles_file: str = None) -> str:
     return "\n".join(lines)
 
 
-def summarize_counters(d: str) -> str:
+def summarize_counters(d: str, roles_file: str = None) -> str:
     """Markdown table per kernel: MFMA busy % (SQ_VALU_MFMA_BUSY_CYCLES over
     GRBM_GUI_ACTIVE / 8 x 1024 SIMDs, pass d/sq) and achieved HBM read / write
     GB/s (copy-calibrated FETCH_SIZE / WRITE_SIZE over the dispatch time,
-    passes d/{fetch,write,cfetch,cwrite})."""
+    passes d/{fetch,write,cfetch,cwrite}). With `roles_file` (the
+    --profile-roles log of the same command as every pass) only the shared
+    step's dispatches are counted."""
     def load(sub):
         rows = {}
         with open(os.path.join(d, sub, "run_counter_collection.csv")) as f:
@@ -266,16 +272,23 @@ def summarize_counters(d: str) -> str:
                 e = rows.setdefault(int(r["Dispatch_Id"]), {"name": r["Kernel_Name"]})
                 e[r["Counter_Name"]] = float(r["Counter_Value"])
                 e["ns"] = int(r["End_Timestamp"]) - int(r["Start_Timestamp"])
-        return rows
-    cf = max(e["FETCH_SIZE"] for e in load("cfetch").values())
-    cw = max(e["WRITE_SIZE"] for e in load("cwrite").values())
+        return [rows[i] for i in sorted(rows)]
+    roles = None
+    if roles_file:
+        with open(roles_file) as f:
+            roles = json.load(f)["launches"]
+    cf = max(e["FETCH_SIZE"] for e in load("cfetch"))
+    cw = max(e["WRITE_SIZE"] for e in load("cwrite"))
     f_scale, w_scale = (1 << 30) / (cf * 1024.0), (1 << 30) / (cw * 1024.0)
     acc = {}
     for sub in ("sq", "fetch", "write"):
-        for e in load(sub).values():
+        lib = [e for e in load(sub) if bench_kernel_name(e["name"]) is not None]
+        if roles is not None:
+            if len(lib) != len(roles):
+                raise ValueError(f"{sub}: {len(lib)} library dispatches but {len(roles)} logged launches")
+            lib = [e for e, r in zip(lib, roles) if r.startswith("shared:")]
+        for e in lib:
             k = bench_kernel_name(e["name"])
-            if k is None:
-                continue
             a = acc.setdefault(k, {"sq_ns": 0, "busy": 0.0, "gui": 0.0, "f_ns": 0, "fb": 0.0, "w_ns": 0, "wb": 0.0,
                                    "n": 0})
             if sub == "sq":
@@ -309,19 +322,20 @@ def summarize_trace(stats_csv: str) -> str:
     return "\n".join(lines)
 
 
-def recorded_traffic(workload: str, kernel: str):
+def recorded_traffic(workload: str, kernel: str, path: str = "tree"):
     """HBM bytes per launch of `kernel` from the committed counter summary of
-    this workload, or None when there is none or the kernel sources changed
-    since the counters were taken."""
-    path = os.path.join(ROOT, "profiles", f"hbm_traffic_{WORKLOAD_SLUG[workload]}.md")
-    if not os.path.exists(path):
+    this workload and step path, or None when there is none or the kernel
+    sources changed since the counters were taken."""
+    fname = os.path.join(ROOT, "profiles", f"hbm_traffic_{WORKLOAD_SLUG[workload]}.md")
+    if not os.path.exists(fname):
         return None
-    with open(path) as f:
+    with open(fname) as f:
         m = re.search(r"<!-- traffic-json (\{.*\}) -->", f.read())
     if not m:
         return None
     data = json.loads(m.group(1))
-    if data.get("source_hash") != kernel_source_hash() or data.get("workload") != workload:
+    if (data.get("source_hash") != kernel_source_hash() or data.get("workload") != workload
+            or data.get("path") != path):
         return None
     k = data["kernels"].get(kernel)
     return None if k is None else k["bytes_per_launch"]
@@ -594,7 +608,8 @@ def main():
     ap.add_argument("--summarize-pmc", default=None, metavar="DIR",
                     help="print the HBM traffic summary of rocprofv3 counter passes in DIR/{fetch,write,cfetch,cwrite} "
                          "(no GPU needed) and exit")
-    ap.add_argument("--roles", default=None, metavar="FILE", help="with --summarize-pmc: the --profile-roles log")
+    ap.add_argument("--roles", default=None, metavar="FILE",
+                    help="with --summarize-pmc / --summarize-counters: the --profile-roles log")
     ap.add_argument("--summarize-counters", default=None, metavar="DIR",
                     help="print MFMA busy %% and achieved HBM GB/s per kernel from rocprofv3 counter passes in "
                          "DIR/{sq,fetch,write,cfetch,cwrite} (no GPU needed) and exit")
@@ -607,7 +622,7 @@ def main():
         print(summarize_pmc(args.summarize_pmc, args.workload, args.roles))
         return
     if args.summarize_counters:
-        print(summarize_counters(args.summarize_counters))
+        print(summarize_counters(args.summarize_counters, args.roles))
         return
     if args.summarize_trace:
         print(summarize_trace(args.summarize_trace))
@@ -713,7 +728,7 @@ def main():
     roof["work_per_launch"] = per_launch
     # HBM bytes per launch measured by the FETCH_SIZE / WRITE_SIZE counter
     # passes (copy-calibrated) on these exact sources, else null
-    roof["traffic"] = recorded_traffic(args.workload, dom_name)
+    roof["traffic"] = recorded_traffic(args.workload, dom_name, args.path)
     roof["traffic_unit"] = "bytes per launch"
     kernel_table = {k: {"ms_per_step": round(v["ms"] / args.steps, 4),
                         ("TFLOP/s" if v["kind"] == "flop" else "GB/s"):

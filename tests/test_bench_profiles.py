@@ -53,7 +53,7 @@ def test_pmc_summary_scales_by_copy_calibration(tmp_path):
 def test_recorded_traffic_requires_matching_sources(tmp_path, monkeypatch):
     prof = tmp_path / "profiles"
     prof.mkdir()
-    data = {"workload": "prompt", "source_hash": bench.kernel_source_hash(),
+    data = {"workload": "prompt", "source_hash": bench.kernel_source_hash(), "path": "tree",
             "kernels": {"attn_dq_kernel": {"bytes_per_launch": 1234}}}
     (prof / "hbm_traffic_prompt_P32768_G8.md").write_text("x\n<!-- traffic-json " + json.dumps(data) + " -->\n")
     monkeypatch.setattr(bench, "ROOT", str(tmp_path))
@@ -63,6 +63,7 @@ def test_recorded_traffic_requires_matching_sources(tmp_path, monkeypatch):
     assert bench.recorded_traffic("prompt", "attn_dq_kernel") == 1234
     assert bench.recorded_traffic("prompt", "attn_fwd_kernel<bf16 out>") is None
     assert bench.recorded_traffic("balanced", "attn_dq_kernel") is None
+    assert bench.recorded_traffic("prompt", "attn_dq_kernel", "calls") is None   # counters of the other path
 
 
 def test_trace_summary(tmp_path):
@@ -123,6 +124,9 @@ def test_pmc_summary_per_role(tmp_path):
     assert r["shared:fwd_replay"]["fetch_bytes_per_launch"] == round(300.0 * 1024 * 2)
     assert r["flattened:fwd_prefill"]["write_bytes_per_launch"] == round(90.0 * 1024)
     assert "shared:dq_replay" in md
+    # the per-kernel figures hold the shared step's dispatches only
+    k = data["kernels"]["attn_fwd_kernel<bf16 out>"]
+    assert k["launches"] == 2 and k["fetch_bytes_per_launch"] == round(200.0 * 1024 * 2)
     roles.write_text(json.dumps({"launches": ["shared:fwd_prefill"]}))
     try:
         bench.summarize_pmc(d, "tiny", str(roles))
