@@ -59,7 +59,7 @@ ROLE_KERNEL = {
     "fwd_tree": "attn_fwd_kernel<bf16 out>", "fwd_replay_split": "attn_fwd_kernel<fp32 out>",
     "dkv_prefill": "attn_dkv_kernel", "dkv_replay": "attn_dkv_kernel", "dkv_tree": "attn_dkv_kernel",
     "dq_prefill": "attn_dq_kernel", "dq_replay": "attn_dq_kernel", "dq_tree": "attn_dq_kernel",
-    "lse_merge": "lse_merge_kernel", "grad_reduce": "grad_reduce_kernel",
+    "lse_merge": "lse_merge_kernel", "grad_reduce": "grad_reduce_kernel", "reduce_tree": "grad_reduce_kernel",
 }
 # launch role -> step of the method (the prefill / replay time breakdown of the
 # six-call path; the two-call path's launches hold both)
@@ -67,13 +67,24 @@ ROLE_STEP = {
     "fwd_prefill": "prefill_fwd", "fwd_replay": "replay_fwd", "fwd_replay_split": "replay_fwd",
     "lse_merge": "replay_fwd", "dkv_replay": "replay_bwd", "dq_replay": "replay_bwd",
     "dkv_prefill": "prefill_bwd", "dq_prefill": "prefill_bwd", "grad_reduce": "prompt_grad_reduce",
-    "fwd_tree": "tree_fwd", "dq_tree": "tree_bwd", "dkv_tree": "tree_bwd",
+    "fwd_tree": "tree_fwd", "dq_tree": "tree_bwd", "dkv_tree": "tree_bwd", "reduce_tree": "tree_bwd",
 }
 # flops per (valid pair, query head) each attention role performs
 ROLE_FLOPS_PER_PAIR_D = {"fwd": 4, "dkv": 8, "dq": 6}
 
 
-def role_work(role: str, shape, n_seed: int, split=None):
+def tree_chunk_rows(shape, chunk_blocks: int) -> int:
+    """fp32 partial rows of the tree backward's chunked prompt-key sweeps:
+    sum over groups of chunks x P when any group is cut into chunks of at most
+    `chunk_blocks` query blocks (64 rows x one query head), else 0."""
+    g = shape.num_q_heads // shape.num_kv_heads
+    n = [min(64, max(1, -(-(-(-sum(rs) // 64) * g) // chunk_blocks))) for rs in shape.branch_lens]
+    if max(n) == 1:
+        return 0
+    return sum(c * p for c, p in zip(n, shape.prompt_lens))
+
+
+def role_work(role: str, shape, n_seed: int, split=None, chunk_blocks: int = 2048):
     """Algorithmic work of one step's launches of a role: ('flop', F) for
     contractions, ('byte', B) for the HBM-bound kernels. `split` flags the
     groups whose replay forward runs SPLIT (None: none of them)."""
@@ -103,6 +114,10 @@ def role_work(role: str, shape, n_seed: int, split=None):
         return "byte", float(e * 4 * (1 + n_seed) + e * 2)
     if role == "lse_merge":
         return "byte", float(rows_split * hq * (2 * d * 4 + 2 * 4 + d * 2 + 4))
+    if role == "reduce_tree":   # the chunks' fp32 partials in, bf16 dK_P / dV_P out
+        v = tree_chunk_rows(shape, chunk_blocks)
+        parts = max(1, -(-v // max(tp, 1)))
+        return "byte", float(2 * v * hkv * d * 4 + parts * tp * 4 + 2 * tp * hkv * d * 2)
     raise KeyError(role)
 
 
@@ -674,6 +689,7 @@ def main():
             for _ in range(args.warmup + args.steps):
                 fstep.run()
             torch.cuda.synchronize()
+        os.makedirs(os.path.dirname(os.path.abspath(args.profile_roles)), exist_ok=True)
         with open(args.profile_roles, "w") as f:
             json.dump({"workload": args.workload, "path": args.path, "launches": log.launches,
                        "flattened_rows": int(fstep.tf)}, f)
@@ -702,7 +718,7 @@ def main():
         kernels, breakdown = {}, {}
         for role, times in kt.summary().items():
             k = ROLE_KERNEL[role]
-            kind, work = role_work(role, s, n_seed, split)
+            kind, work = role_work(role, s, n_seed, split, lib.augtree_tree_chunk_blocks())
             e = kernels.setdefault(k, {"ms": 0.0, "launches": 0, "work": 0.0, "kind": kind})
             e["ms"] += float(np.sum(times))
             e["launches"] += len(times)

@@ -260,16 +260,24 @@ int augtree_tree_fwd(const augtree_groups* grp, int mode, const uint16_t* q_p, c
  *     the prompt queries' own contribution) is accumulated in registers, in
  *     that fixed order, and rounded once; each branch-key tile sweeps its
  *     branch's rows (causal).
+ * A group whose branch rows exceed augtree_tree_chunk_blocks() query blocks
+ * (64 rows of one query head) per prompt-key tile has that sweep cut into
+ * chunks (at most 64) of consecutive branch rows, the first chunk also taking
+ * the prompt rows; the chunks write fp32 partial sums to the workspace and a
+ * third launch adds them per row in chunk order and rounds once (role
+ * "reduce_tree"). Long sweeps otherwise lose the L2 sharing of the query rows.
  * The prompt gradient is the same sum as the three-call path up to fp32
  * rounding order (that path adds two fp32 partial sums); it is bitwise
- * reproducible. dQ carries the same common-mode correction as
- * augtree_replay_bwd.
+ * reproducible for a given chunk setting. dQ carries the same common-mode
+ * correction as augtree_replay_bwd.
  * In:  q_p, k_p, v_p, o_p (bf16), lse_p (fp32), do_p (bf16) [prompt rows];
  *      q_r, k_r, v_r, o_r (bf16), lse_r (fp32), do_r (bf16) [response rows].
  * Out: dq_p [T_P,Hq,d], dk_p, dv_p [T_P,Hkv,d], dq_r [T_R,Hq,d], dk_r, dv_r
  *      [T_R,Hkv,d] bf16; dkv_p_f32 [2][T_P,Hkv,d] fp32 (nullable: the prompt
  *      gradient before its bf16 rounding, 0 = dK, 1 = dV).
- * Workspace: augtree_workspace_size(grp, AUGTREE_OP_TREE_BWD, 0).
+ * Workspace: augtree_workspace_size(grp, AUGTREE_OP_TREE_BWD, 0) (with chunks:
+ * the fp32 partials, 2 x (sum over chunked groups of chunks x P) x Hkv x d x 4
+ * bytes, and a row map of chunks x T_P int32).
  */
 int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p,
                      const uint16_t* v_p, const uint16_t* o_p, const float* lse_p,
@@ -283,12 +291,15 @@ int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint1
  * augtree_tree_bwd without a workspace argument, for callers that cannot
  * allocate device memory (code under stream capture, tight serving loops,
  * harnesses that forbid allocation). Same inputs, outputs and results as
- * augtree_tree_bwd (bit for bit: same kernels and schedule). Its workspace is
+ * augtree_tree_bwd (bit for bit: same kernels and schedule, except that a
+ * batch whose chunked schedule does not fit the array runs one sweep per
+ * prompt-key tile: the same prompt gradient up to fp32 summation order). Its
+ * workspace is
  * a fixed 64 MiB device array of the library (augtree_noalloc_scratch_bytes()),
  * one copy per GPU, held from the first call on that GPU until the process
- * ends; the call performs no allocation. A batch whose workspace
- * (augtree_workspace_size(grp, AUGTREE_OP_TREE_BWD, 0)) exceeds it is rejected
- * with AUGTREE_ERR_WORKSPACE before anything is enqueued. Calls that overlap on
+ * ends; the call performs no allocation. A batch whose unchunked workspace
+ * exceeds it is rejected with AUGTREE_ERR_WORKSPACE before anything is
+ * enqueued. Calls that overlap on
  * one GPU (several streams or threads) share the array and race; serialise
  * them.
  */
@@ -336,13 +347,23 @@ int augtree_prompt_grad_reduce(int32_t n_tensors, int64_t rows, int32_t heads, i
  * (phase 1) every kernel launch the library enqueues from that thread, with a
  * static role name ("fwd_prefill", "fwd_replay", "fwd_tree", "fwd_replay_split",
  * "lse_merge", "dq_prefill", "dkv_prefill", "dq_replay", "dkv_replay", "dq_tree",
- * "dkv_tree", "grad_reduce") and the stream the
+ * "dkv_tree", "grad_reduce", "reduce_tree") and the stream the
  * kernel is enqueued on, so that a caller can record HIP events around single
  * kernels. The hook must not call back into the library. NULL removes it.
  * Per thread; the library keeps no other state.
  */
 typedef void (*augtree_launch_hook)(const char* role, int phase, void* stream, void* user);
 void augtree_set_launch_hook(augtree_launch_hook hook, void* user);
+
+/*
+ * Tuning of augtree_tree_bwd (process-wide; schedules and workspace sizes
+ * computed after the call use it): the most query blocks (64 rows x one
+ * query head) one prompt-key tile sweeps over a group's branch rows before
+ * the sweep is cut into chunks. blocks >= 1 sets it, 0 restores the default
+ * (2048); negative: AUGTREE_ERR_INVALID_ARGUMENT.
+ */
+int augtree_set_tree_chunk_blocks(int32_t blocks);
+int32_t augtree_tree_chunk_blocks(void);
 
 /* Static text of a status code. */
 const char* augtree_status_string(int status);

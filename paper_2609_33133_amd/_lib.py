@@ -37,7 +37,7 @@ EXPORTS = (
     "augtree_replay_bwd", "augtree_prefill_bwd", "augtree_prompt_grad_reduce", "augtree_status_string",
     "augtree_last_error", "augtree_check_device", "augtree_version", "augtree_set_launch_hook",
     "augtree_replay_split_groups", "augtree_tree_fwd", "augtree_tree_bwd", "augtree_tree_bwd_noalloc",
-    "augtree_noalloc_scratch_bytes",
+    "augtree_noalloc_scratch_bytes", "augtree_set_tree_chunk_blocks", "augtree_tree_chunk_blocks",
 )
 
 LAUNCH_HOOK = ctypes.CFUNCTYPE(None, ctypes.c_char_p, ctypes.c_int, ctypes.c_void_p, ctypes.c_void_p)
@@ -92,6 +92,8 @@ def _sig(lib):
         "augtree_tree_bwd": (ctypes.c_int, [_GP] + [_P] * 19 + [_P, _SZ, _P]),
         "augtree_tree_bwd_noalloc": (ctypes.c_int, [_GP] + [_P] * 19 + [_P]),
         "augtree_noalloc_scratch_bytes": (_SZ, []),
+        "augtree_set_tree_chunk_blocks": (ctypes.c_int, [_I32]),
+        "augtree_tree_chunk_blocks": (_I32, []),
     }
     for name, (res, args) in sigs.items():
         fn = getattr(lib, name)

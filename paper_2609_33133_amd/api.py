@@ -129,6 +129,18 @@ def replay_split_groups(b: GroupBatch) -> np.ndarray:
     return out
 
 
+def set_tree_chunk_blocks(blocks: int) -> None:
+    """Most query blocks (64 rows x one query head) a prompt-key tile of the
+    tree backward sweeps over a group's branch rows before the sweep is cut
+    into chunks (0 restores the default). Process-wide; workspaces sized
+    afterwards follow it."""
+    _lib.check(_lib.load().augtree_set_tree_chunk_blocks(int(blocks)), "set_tree_chunk_blocks")
+
+
+def tree_chunk_blocks() -> int:
+    return int(_lib.load().augtree_tree_chunk_blocks())
+
+
 def lse_merge(o_parts, lse_parts, o=None, o_f32=None, lse=None, want_bf16=True, stream=None):
     n, rows, heads, d = o_parts.shape
     _need(o_parts, "o_parts", torch.float32, (n, rows, heads, d))

@@ -343,7 +343,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   const int64_t st_rows[2] = {p.lse_rows[0], p.lse_rows[1]};
   auto load_block = [&](int b, __bf16* qd, __bf16* od) {
     const Blk k = block_of(b);
-    const int64_t row0 = (int64_t)(k.y ? t.y_row0 : t.x_row0) + k.qb * KV_BQ;
+    const int64_t row0 = (int64_t)(k.y ? t.kv_row0 : t.x_row0) + k.qb * KV_BQ;
     const int nvalid = min(KV_BQ, (k.y ? t.y_len : t.x_len) - k.qb * KV_BQ);
     qc.issue(qd, k.y ? q_src[1] : q_src[0], row0, nvalid, qstride, k.hh * D);
     qc.issue(od, k.y ? do_src[1] : do_src[0], row0, nvalid, qstride, k.hh * D);
@@ -477,19 +477,20 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   uint16_t* const dk16 = (t.flags & KV_OUT_BF16) ? p.dk[pk] : nullptr;
   uint16_t* const dv16 = (t.flags & KV_OUT_BF16) ? p.dv[pk] : nullptr;
   const int64_t slab = p.slab_rows * kvstride;
-  float* const dk32 = (t.flags & KV_OUT_SLAB) ? p.slab + 2 * (int64_t)(t.flags >> KV_PART_SHIFT) * slab : nullptr;
+  float* const dk32 = (t.flags & KV_OUT_SLAB) ? p.slab + (int64_t)t.out_row0 * kvstride : nullptr;
 #pragma unroll
   for (int db = 0; db < D / 32; ++db) {
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       const int key = kw0 + acc_row(i, hf);
       if (key < t.kv_len) {
-        const int64_t row = (int64_t)t.kv_row0 + key;
-        const int64_t off = row * kvstride + kvh * D + db * 32 + l32;
+        const int64_t col = kvh * D + db * 32 + l32;
+        const int64_t off = ((int64_t)t.kv_row0 + key) * kvstride + col;
         const float kval = dk[db][i] * p.scale, vval = dv[db][i];
         if (dk32) {
-          dk32[off] = kval;
-          dk32[slab + off] = vval;
+          const int64_t so = (int64_t)key * kvstride + col;
+          dk32[so] = kval;
+          dk32[slab + so] = vval;
         }
         if (dk16) {
           reinterpret_cast<__bf16*>(dk16)[off] = (__bf16)kval;

@@ -321,11 +321,12 @@ std::vector<char> replay_split_groups(const Shape& s, int mode) {
   return v;
 }
 
-// prompt key tiles of every group: X = response rows r0 + x0 .. r0 + x1 - 1
-// of the group (all branches; every prompt key visible), Y = the prefill rows
-// from the tile's first key (causal) if `prefill`
+// prompt key tiles of group g: X = response rows r0 + x0 .. r0 + x1 - 1 of
+// the group (all branches; every prompt key visible), Y = the prefill rows
+// from the tile's first key (causal) if `prefill`; with KV_OUT_SLAB, the fp32
+// result of the group's key k goes to slab row out_base + k
 void add_prompt_kvtiles(TileList<KVTile>& L, const Shape& s, int bn, int g, int x0, int x1, bool prefill,
-                        int32_t flags) {
+                        int32_t flags, int64_t out_base = 0) {
   const int P = s.cp[g + 1] - s.cp[g];
   // (a prefill-only call passes no branch offsets and an empty X range)
   const int r0 = x1 > x0 ? s.cr[s.cb[g]] : 0;
@@ -335,11 +336,9 @@ void add_prompt_kvtiles(TileList<KVTile>& L, const Shape& s, int bn, int g, int 
     t.kv_len = std::min(bn, P - k0);
     t.x_row0 = r0 + x0;
     t.x_len = x1 - x0;
-    if (prefill) {
-      t.y_row0 = s.cp[g] + k0;  // queries before the first key cannot see it
-      t.y_len = P - k0;
-    }
+    if (prefill) t.y_len = P - k0;  // queries before the first key cannot see it
     t.kpos0 = k0;
+    t.out_row0 = (flags & KV_OUT_SLAB) ? (int32_t)(out_base + k0) : 0;
     t.flags = flags | KV_PROMPT_KEYS;
     L.add(t, g);
   }
@@ -361,6 +360,13 @@ void add_response_kvtiles(TileList<KVTile>& L, const Shape& s, int bn) {
     }
   }
 }
+
+// The tree backward cuts a prompt key tile's sweep over the branch rows into
+// chunks of at most this many query blocks (64 rows of one query head): the
+// workgroups that share the same query rows drift apart over long sweeps, and
+// then neither they nor the branch key tiles running beside them find those
+// rows in L2.
+std::atomic<int> g_tree_chunk_blocks{kTreeChunkBlocksDefault};
 
 // Boundaries of chunk c of n of a group's `nr` response rows, on multiples of
 // the query block where possible.
@@ -387,6 +393,13 @@ struct Plan {
   TileList<KVTile> kv;
   size_t off_q[3] = {0, 0, 0}, off_kv = 0, off_dsum_p = 0, off_dsum_r = 0, bytes = 0, blob_bytes = 0;
   int64_t dsum_rows_p = 0, dsum_rows_r = 0;
+  // chunked prompt-key sweeps of the tree backward (n_parts > 0): the fp32
+  // slab [2][slab_rows, Hkv, d] of the chunks and the reduce's row map
+  // [n_parts][T_P] (uploaded with the schedules)
+  int n_parts = 0;
+  int64_t slab_rows = 0;
+  std::vector<int32_t> row_map;
+  size_t off_row_map = 0, off_slab = 0;
   std::vector<char> blob;
 
   void sort(const Shape& s) {
@@ -395,7 +408,7 @@ struct Plan {
   }
   // every list gets room in the workspace (its size does not depend on
   // which lists end up inline)
-  void layout(int hq) {
+  void layout(int hq, int64_t row_elems) {
     size_t o = 0;
     for (int i = 0; i < 3; ++i) {
       off_q[i] = o;
@@ -403,11 +416,15 @@ struct Plan {
     }
     off_kv = o;
     o = align_up(o + kv.v.size() * sizeof(KVTile));
+    off_row_map = o;
+    o = align_up(o + row_map.size() * sizeof(int32_t));
     blob_bytes = o;
     off_dsum_p = o;
     o = align_up(o + (size_t)dsum_rows_p * hq * sizeof(float));
     off_dsum_r = o;
     o = align_up(o + (size_t)dsum_rows_r * hq * sizeof(float));
+    off_slab = o;
+    o = align_up(o + (size_t)slab_rows * 2 * row_elems * sizeof(float));
     bytes = std::max<size_t>(o, kAlign);
   }
   static bool inline_list(size_t n) { return n <= (size_t)kInlineTiles; }
@@ -417,6 +434,7 @@ struct Plan {
     for (int i = 0; i < 3; ++i)
       if (!inline_list(q[i].v.size())) end = off_q[i] + q[i].v.size() * sizeof(QTile);
     if (!inline_list(kv.v.size())) end = off_kv + kv.v.size() * sizeof(KVTile);
+    if (!row_map.empty()) end = off_row_map + row_map.size() * sizeof(int32_t);
     return end;
   }
   void pack() {
@@ -425,6 +443,7 @@ struct Plan {
       if (!inline_list(q[i].v.size()))
         std::memcpy(blob.data() + off_q[i], q[i].v.data(), q[i].v.size() * sizeof(QTile));
     if (!inline_list(kv.v.size())) std::memcpy(blob.data() + off_kv, kv.v.data(), kv.v.size() * sizeof(KVTile));
+    if (!row_map.empty()) std::memcpy(blob.data() + off_row_map, row_map.data(), row_map.size() * sizeof(int32_t));
   }
 };
 
@@ -463,7 +482,7 @@ Plan plan_for(const Shape& s, int op, int arg) {
     }
     case AUGTREE_OP_PREFILL_BWD:
       add_prefill_qtiles(pl.q[0], s, dq_block_m());
-      for (int g = 0; g < s.ng; ++g) add_prompt_kvtiles(pl.kv, s, bn, g, 0, 0, true, KV_OUT_SLAB);
+      for (int g = 0; g < s.ng; ++g) add_prompt_kvtiles(pl.kv, s, bn, g, 0, 0, true, KV_OUT_SLAB, s.cp[g]);
       pl.dsum_rows_p = s.tp;
       break;
     case AUGTREE_OP_REPLAY_BWD:
@@ -473,19 +492,53 @@ Plan plan_for(const Shape& s, int op, int arg) {
         const int64_t nr = s.cr[s.cb[g + 1]] - s.cr[s.cb[g]];
         for (int c = 0; c < arg; ++c) {
           const int c0 = seed_edge(nr, c, arg, bq), c1 = std::max(seed_edge(nr, c + 1, arg, bq), c0);
-          add_prompt_kvtiles(pl.kv, s, bn, g, c0, c1, false, KV_OUT_SLAB | (c << KV_PART_SHIFT));
+          // seed slab layout [part][2][T_P]
+          add_prompt_kvtiles(pl.kv, s, bn, g, c0, c1, false, KV_OUT_SLAB, 2 * (int64_t)c * s.tp + s.cp[g]);
         }
       }
       pl.dsum_rows_r = s.tr;
       break;
     case AUGTREE_OP_TREE_BWD: {
+      // arg bit 0: the fp32 copy of the prompt-key gradient is requested too;
+      // bit 1: no chunked prompt-key sweeps (keeps the workspace small)
       add_prefill_qtiles(pl.q[0], s, dq_block_m());
       add_replay_qtiles(pl.q[0], s, dq_block_m(), RP_FUSED);
       add_response_kvtiles(pl.kv, s, bn);
-      // arg != 0: the fp32 copy of the prompt-key gradient is requested too
-      const int32_t out = KV_OUT_BF16 | (arg ? KV_OUT_SLAB : 0);
-      for (int g = 0; g < s.ng; ++g)
-        add_prompt_kvtiles(pl.kv, s, bn, g, 0, s.cr[s.cb[g + 1]] - s.cr[s.cb[g]], true, out);
+      std::vector<int> nc(s.ng, 1);
+      int nmax = 1;
+      if (!(arg & 2))
+        for (int g = 0; g < s.ng; ++g) {
+          nc[g] = tree_chunk_count(s.cr[s.cb[g + 1]] - s.cr[s.cb[g]], s.group);
+          nmax = std::max(nmax, nc[g]);
+        }
+      if (nmax == 1) {
+        // one sweep per prompt key tile: the Eq. 2 sum stays in registers and
+        // the tile writes bf16 (and the caller's fp32 copy, [2][T_P])
+        const int32_t out = KV_OUT_BF16 | ((arg & 1) ? KV_OUT_SLAB : 0);
+        for (int g = 0; g < s.ng; ++g)
+          add_prompt_kvtiles(pl.kv, s, bn, g, 0, s.cr[s.cb[g + 1]] - s.cr[s.cb[g]], true, out, s.cp[g]);
+      } else {
+        // chunk c of group g sweeps its share of the branch rows (chunk 0
+        // also the prefill rows) into the fp32 rows vbase_g + c P_g + key of
+        // a workspace slab; the reduce adds the chunks in order
+        std::vector<int64_t> vbase(s.ng + 1, 0);
+        for (int g = 0; g < s.ng; ++g) vbase[g + 1] = vbase[g] + (int64_t)nc[g] * (s.cp[g + 1] - s.cp[g]);
+        if (vbase[s.ng] > INT32_MAX) return plan_for(s, op, arg | 2);  // slab rows are int32
+        for (int g = 0; g < s.ng; ++g) {
+          const int64_t P = s.cp[g + 1] - s.cp[g], nr = s.cr[s.cb[g + 1]] - s.cr[s.cb[g]];
+          for (int c = 0; c < nc[g]; ++c) {
+            const int c0 = seed_edge(nr, c, nc[g], bq), c1 = std::max(seed_edge(nr, c + 1, nc[g], bq), c0);
+            add_prompt_kvtiles(pl.kv, s, bn, g, c0, c1, c == 0, KV_OUT_SLAB, vbase[g] + c * P);
+          }
+        }
+        pl.n_parts = nmax;
+        pl.slab_rows = vbase[s.ng];
+        pl.row_map.assign((size_t)nmax * s.tp, -1);
+        for (int g = 0; g < s.ng; ++g)
+          for (int c = 0; c < nc[g]; ++c)
+            for (int32_t r = s.cp[g]; r < s.cp[g + 1]; ++r)
+              pl.row_map[(size_t)c * s.tp + r] = (int32_t)(vbase[g] + (int64_t)c * (s.cp[g + 1] - s.cp[g]) + r - s.cp[g]);
+      }
       pl.dsum_rows_p = s.tp;
       pl.dsum_rows_r = s.tr;
       break;
@@ -494,7 +547,7 @@ Plan plan_for(const Shape& s, int op, int arg) {
       break;
   }
   pl.sort(s);
-  pl.layout(s.hq);
+  pl.layout(s.hq, (int64_t)s.hkv * s.d);
   return pl;
 }
 
@@ -653,6 +706,14 @@ void augtree_set_launch_hook(augtree_launch_hook hook, void* user) {
   g_hook_user = user;
 }
 
+int augtree_set_tree_chunk_blocks(int32_t blocks) {
+  if (blocks < 0) return fail(AUGTREE_ERR_INVALID_ARGUMENT, "chunk blocks %d < 0", blocks);
+  g_tree_chunk_blocks.store(blocks == 0 ? kTreeChunkBlocksDefault : blocks, std::memory_order_relaxed);
+  return ok();
+}
+
+int32_t augtree_tree_chunk_blocks(void) { return g_tree_chunk_blocks.load(std::memory_order_relaxed); }
+
 int augtree_check_device(void) {
   const int st = check_device_impl();
   return st == AUGTREE_OK ? ok() : st;
@@ -781,6 +842,8 @@ int augtree_replay_bwd(const augtree_groups* grp, const uint16_t* q_r, const uin
   int st = validate_groups(grp, &s);
   if (st) return st;
   if (n_seed < 1 || n_seed > 64) return fail(AUGTREE_ERR_INVALID_ARGUMENT, "n_seed %d not in [1,64]", n_seed);
+  if (2 * (int64_t)n_seed * s.tp > INT32_MAX)
+    return fail(AUGTREE_ERR_UNSUPPORTED, "seed slab of %d x 2 x %lld rows exceeds int32 rows", n_seed, (long long)s.tp);
   REQUIRE_PTR(q_r); REQUIRE_PTR(k_r); REQUIRE_PTR(v_r); REQUIRE_PTR(k_p); REQUIRE_PTR(v_p);
   REQUIRE_PTR(o_r); REQUIRE_PTR(lse_r); REQUIRE_PTR(do_r);
   REQUIRE_PTR(dq_r); REQUIRE_PTR(dk_r); REQUIRE_PTR(dv_r); REQUIRE_PTR(dkv_p_seed);
@@ -829,6 +892,12 @@ namespace augtree {
 
 int fail_status(int status, const char* msg) { return fail(status, "%s", msg); }
 
+int tree_chunk_count(int64_t nr, int group) {
+  const int64_t blocks = (nr + kDkvBlockQ - 1) / kDkvBlockQ * group;
+  const int64_t per = g_tree_chunk_blocks.load(std::memory_order_relaxed);
+  return (int)std::min<int64_t>(64, std::max<int64_t>(1, (blocks + per - 1) / per));
+}
+
 int tree_bwd_impl(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p, const uint16_t* v_p,
                   const uint16_t* o_p, const float* lse_p, const uint16_t* do_p, const uint16_t* q_r,
                   const uint16_t* k_r, const uint16_t* v_r, const uint16_t* o_r, const float* lse_r,
@@ -844,6 +913,9 @@ int tree_bwd_impl(const augtree_groups* grp, const uint16_t* q_p, const uint16_t
   OPTIONAL_PTR(dkv_p_f32);
   Plan pl = plan_for(s, AUGTREE_OP_TREE_BWD, dkv_p_f32 ? 1 : 0);
   if (scratch) {  // the caller's buffer is a fixed device array: check its size before touching the device
+    // chunked prompt-key sweeps need an fp32 slab; without room for it, one
+    // sweep per prompt key tile (the same sum in another fp32 order)
+    if (pl.bytes > ws_bytes && pl.n_parts > 0) pl = plan_for(s, AUGTREE_OP_TREE_BWD, (dkv_p_f32 ? 1 : 0) | 2);
     if (pl.bytes > ws_bytes)
       return fail(AUGTREE_ERR_WORKSPACE,
                   "this batch needs %zu bytes of scratch; the allocation-free entry point holds at most %zu bytes",
@@ -859,8 +931,26 @@ int tree_bwd_impl(const augtree_groups* grp, const uint16_t* q_p, const uint16_t
   BwdOut out{};
   out.dq_p = dq_p; out.dq_r = dq_r;
   out.dk_p = dk_p; out.dv_p = dv_p; out.dk_r = dk_r; out.dv_r = dv_r;
-  out.slab = dkv_p_f32; out.slab_rows = s.tp;
+  if (pl.n_parts > 0) {
+    out.slab = reinterpret_cast<float*>(static_cast<char*>(ws) + pl.off_slab);
+    out.slab_rows = pl.slab_rows;
+  } else {
+    out.slab = dkv_p_f32;
+    out.slab_rows = s.tp;
+  }
   if ((st = run_bwd(s, pl, x, out, ws, str, "dq_tree", "dkv_tree"))) return st;
+  if (pl.n_parts > 0) {
+    // the chunks of each prompt key row, added in chunk order (Eq. 2)
+    const int64_t e = (int64_t)s.hkv * s.d;
+    uint16_t* const o16[2] = {dk_p, dv_p};
+    float* const o32[2] = {dkv_p_f32, dkv_p_f32 ? dkv_p_f32 + s.tp * e : nullptr};
+    HookScope h("reduce_tree", str);
+    if ((st = hip_status(launch_grad_reduce(2, s.tp, e, nullptr, pl.n_parts, pl.slab_rows, 0, out.slab,
+                                            reinterpret_cast<const int32_t*>(static_cast<char*>(ws) + pl.off_row_map),
+                                            o16, o32, str),
+                         "reduce launch")))
+      return st;
+  }
   return ok();
 }
 
@@ -896,8 +986,11 @@ int augtree_prompt_grad_reduce(int32_t n_tensors, int64_t rows, int32_t heads, i
   int st;
   if ((st = check_device_impl())) return st;
   HookScope h("grad_reduce", static_cast<hipStream_t>(stream));
-  if ((st = hip_status(launch_grad_reduce(n_tensors, rows, (int64_t)heads * head_dim, self, n_parts, part_rows,
-                                          part_stride, parts, row_map, out, out_f32, static_cast<hipStream_t>(stream)),
+  const int64_t e = (int64_t)heads * head_dim;
+  uint16_t* const o16[2] = {out, out && n_tensors > 1 ? out + rows * e : nullptr};
+  float* const o32[2] = {out_f32, out_f32 && n_tensors > 1 ? out_f32 + rows * e : nullptr};
+  if ((st = hip_status(launch_grad_reduce(n_tensors, rows, e, self, n_parts, part_rows, part_stride, parts, row_map,
+                                          o16, o32, static_cast<hipStream_t>(stream)),
                        "grad reduce launch")))
     return st;
   return ok();

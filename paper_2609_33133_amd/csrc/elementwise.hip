@@ -72,7 +72,8 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(int n_tensors, int64_t
                                                           int64_t part_rows, int64_t part_stride,
                                                           const float* __restrict__ parts,
                                                           const int32_t* __restrict__ row_map,
-                                                          uint16_t* __restrict__ out, float* __restrict__ out32) {
+                                                          uint16_t* out0, uint16_t* out1, float* o32_0,
+                                                          float* o32_1) {
   const int64_t q_per_row = row_elems / 4;
   const int64_t total = (int64_t)n_tensors * rows * q_per_row;
   for (int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; gid < total;
@@ -89,11 +90,13 @@ __global__ __launch_bounds__(256) void grad_reduce_kernel(int n_tensors, int64_t
           *reinterpret_cast<const float4*>(parts + (int64_t)k * part_stride + (tsr * part_rows + src) * row_elems + e);
       acc.x += v.x; acc.y += v.y; acc.z += v.z; acc.w += v.w;
     }
-    if (out32) *reinterpret_cast<float4*>(out32 + tr * row_elems + e) = acc;
+    float* const out32 = tsr ? o32_1 : o32_0;
+    uint16_t* const out = tsr ? out1 : out0;
+    if (out32) *reinterpret_cast<float4*>(out32 + row * row_elems + e) = acc;
     if (out) {
       bf16x4 w;
       w[0] = (__bf16)acc.x; w[1] = (__bf16)acc.y; w[2] = (__bf16)acc.z; w[3] = (__bf16)acc.w;
-      *reinterpret_cast<bf16x4*>(out + tr * row_elems + e) = w;
+      *reinterpret_cast<bf16x4*>(out + row * row_elems + e) = w;
     }
   }
 }
@@ -117,12 +120,13 @@ hipError_t launch_lse_merge(int64_t row0, int64_t rows, int64_t total_rows, int 
 }
 
 hipError_t launch_grad_reduce(int n_tensors, int64_t rows, int64_t row_elems, const float* self, int n_parts,
-                              int64_t part_rows, int64_t part_stride, const float* parts, const int32_t* row_map, uint16_t* out,
-                              float* out32, hipStream_t stream) {
+                              int64_t part_rows, int64_t part_stride, const float* parts, const int32_t* row_map,
+                              uint16_t* const out[2], float* const out32[2], hipStream_t stream) {
   const int64_t threads = (int64_t)n_tensors * rows * (row_elems / 4);
   if (threads == 0) return hipSuccess;
   hipLaunchKernelGGL(grad_reduce_kernel, dim3(grid_for(threads)), dim3(256), 0, stream, n_tensors, rows,
-                     row_elems, self, n_parts, part_rows, part_stride, parts, row_map, out, out32);
+                     row_elems, self, n_parts, part_rows, part_stride, parts, row_map, out[0], out[1], out32[0],
+                     out32[1]);
   return hipGetLastError();
 }
 

@@ -26,4 +26,10 @@ int tree_bwd_impl(const augtree_groups* grp, const uint16_t* q_p, const uint16_t
 // Records `msg` as the calling thread's last error; returns `status`.
 int fail_status(int status, const char* msg);
 
+// Chunks of the tree backward's prompt-key sweep over a group's `nr` branch
+// rows (each chunk at most augtree_set_tree_chunk_blocks query blocks of 64
+// rows x one of the `group` query heads; between 1 and 64).
+constexpr int kTreeChunkBlocksDefault = 2048;
+int tree_chunk_count(int64_t nr, int group);
+
 }  // namespace augtree

@@ -65,7 +65,7 @@ struct DkvParams {
   int64_t lse_rows[2];
   uint16_t* dk[2];            // bf16 outputs [*, hkv, d] (KV_OUT_BF16)
   uint16_t* dv[2];
-  float* slab;                // fp32 slabs [part][2][slab_rows, hkv, d] (KV_OUT_SLAB)
+  float* slab;                // fp32 slab [2][slab_rows, hkv, d] (KV_OUT_SLAB; rows per tile: out_row0)
   int64_t slab_rows;
   int hq, hkv, group, head_dim;
   float scale, scale_log2;
@@ -79,9 +79,12 @@ hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, hipStream_t stream);
 hipError_t launch_lse_merge(int64_t row0, int64_t rows, int64_t total_rows, int heads, int head_dim, int n_parts,
                             const float* o_parts, const float* lse_parts, uint16_t* o, float* o32, float* lse,
                             hipStream_t stream);
+// out[t][row] = self[t][row] + sum over k of parts[k][t][src(k, row)] (src =
+// row, or row_map[k * rows + row], skipped when negative), tensors t < n_tensors
+// written to out[t] (bf16) and/or out32[t] (fp32), each [rows, row_elems]
 hipError_t launch_grad_reduce(int n_tensors, int64_t rows, int64_t row_elems, const float* self, int n_parts,
-                              int64_t part_rows, int64_t part_stride, const float* parts, const int32_t* row_map, uint16_t* out,
-                              float* out32, hipStream_t stream);
+                              int64_t part_rows, int64_t part_stride, const float* parts, const int32_t* row_map,
+                              uint16_t* const out[2], float* const out32[2], hipStream_t stream);
 
 inline int fwd_block_m() { return kFwdBlockM; }
 inline int fwd_block_n() { return kFwdBlockN; }

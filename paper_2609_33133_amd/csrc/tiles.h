@@ -40,17 +40,20 @@ enum : int32_t {
 // two ranges of query rows, swept in this order:
 //   X: response rows x_row0 .. x_row0 + x_len - 1 (Q_R, dO_R, LSE_R, D_R),
 //      causal if KV_X_CAUSAL, otherwise every key visible;
-//   Y: prompt rows y_row0 .. y_row0 + y_len - 1 (Q_P, ...), causal.
+//   Y: prompt rows kv_row0 .. kv_row0 + y_len - 1 (Q_P, ...), causal (prompt
+//      keys only: prompt queries before the tile's first key cannot see it).
 // In a causal range, query i sits at position kpos0 + i of its segment (the
 // range starts at the tile's first key) and key j at kpos0 + j: visible iff
-// j <= i. Outputs: the key rows' dK/dV, in bf16 (KV_OUT_BF16) and/or into
-// fp32 slab `part` (KV_OUT_SLAB).
+// j <= i. Outputs: the key rows' dK/dV in bf16 (KV_OUT_BF16, rows kv_row0 ..)
+// and/or fp32 (KV_OUT_SLAB): dK of key j at row out_row0 + j of the fp32 slab,
+// dV slab_rows rows further on.
 struct KVTile {
   int32_t kv_row0, kv_len;
   int32_t x_row0, x_len;
-  int32_t y_row0, y_len;
+  int32_t y_len;
   int32_t kpos0;
-  int32_t flags;  // KV_* | part << KV_PART_SHIFT
+  int32_t out_row0;
+  int32_t flags;  // KV_*
 };
 
 enum : int32_t {
@@ -58,7 +61,6 @@ enum : int32_t {
   KV_X_CAUSAL = 2,
   KV_OUT_BF16 = 4,
   KV_OUT_SLAB = 8,
-  KV_PART_SHIFT = 8,
 };
 
 }  // namespace augtree

@@ -39,6 +39,11 @@ bool fail_now() { return g_fail_at > 0 && ++g_calls == g_fail_at; }
 
 // coverage of output rows: key = (output name), value = per-row write count
 std::map<std::string, std::vector<int>> g_cov;
+// fp32 slab rows written by dK/dV tiles (KV_OUT_SLAB), by slab row
+std::vector<int> g_slab;
+// the workspace of the entry point under test (host memory here)
+const char* g_ws = nullptr;
+size_t g_ws_bytes = 0;
 
 void cover(const std::string& name, int64_t rows, int64_t r0, int64_t n) {
   auto& v = g_cov[name];
@@ -72,6 +77,7 @@ int64_t seg_start(const std::vector<int32_t>& cu, int64_t r0, int64_t n) {
 void fake_set_shape(const FakeShape& s) {
   g_shape = s;
   g_cov.clear();
+  g_slab.clear();
   g_counts = FakeCounts{};
   g_errors.clear();
 }
@@ -95,7 +101,15 @@ void fake_check_coverage(const char* name, int64_t rows) {
       return;
     }
 }
-void fake_reset_coverage() { g_cov.clear(); }
+void fake_reset_coverage() {
+  g_cov.clear();
+  g_slab.clear();
+}
+void fake_set_workspace(const void* ws, size_t bytes) {
+  g_ws = static_cast<const char*>(ws);
+  g_ws_bytes = bytes;
+}
+const std::vector<int>& fake_slab_rows() { return g_slab; }
 
 // ------------------------------------------------------------------ HIP runtime
 
@@ -176,7 +190,7 @@ hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, hipStream_t) {
     if (t.kpos0 != t.kv_row0 - kstart) err("dkv: key position");
     if (t.x_len > 0 && (t.x_row0 < 0 || t.x_row0 + t.x_len > s.tr)) err("dkv: response rows out of range");
     if (t.y_len > 0) {
-      if (!pk || t.y_row0 != t.kv_row0 || seg_start(s.cu_prompt, t.y_row0, t.y_len) < 0) err("dkv: prompt rows");
+      if (!pk || seg_start(s.cu_prompt, t.kv_row0, t.y_len) < 0) err("dkv: prompt rows");
     }
     if ((t.flags & KV_X_CAUSAL) && (pk || t.x_row0 != t.kv_row0 || seg_start(s.cu_resp, t.x_row0, t.x_len) < 0))
       err("dkv: causal response rows");
@@ -186,8 +200,9 @@ hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, hipStream_t) {
       cover(pk ? "dk_p" : "dk_r", rows, t.kv_row0, t.kv_len);
     }
     if (t.flags & KV_OUT_SLAB) {
-      if (!p.slab || p.slab_rows != s.tp || !pk) err("dkv: slab output");
-      cover("slab" + std::to_string(t.flags >> KV_PART_SHIFT), rows, t.kv_row0, t.kv_len);
+      if (!p.slab || !pk || t.out_row0 < 0 || t.out_row0 + t.kv_len > p.slab_rows * 64) err("dkv: slab output");
+      if ((int64_t)g_slab.size() < (int64_t)t.out_row0 + t.kv_len) g_slab.resize(t.out_row0 + t.kv_len, 0);
+      for (int j = 0; j < t.kv_len; ++j) g_slab[t.out_row0 + j] += 1;
     }
     for (int j = 0; j < t.kv_len; ++j) {
       const int64_t xs = (t.flags & KV_X_CAUSAL) ? std::max<int64_t>(0, t.x_len - j) : t.x_len;
@@ -208,10 +223,39 @@ hipError_t launch_lse_merge(int64_t row0, int64_t rows, int64_t total_rows, int,
   return hipSuccess;
 }
 
-hipError_t launch_grad_reduce(int n_tensors, int64_t rows, int64_t, const float*, int n_parts, int64_t, int64_t,
-                              const float*, const int32_t*, uint16_t*, float*, hipStream_t) {
+hipError_t launch_grad_reduce(int n_tensors, int64_t rows, int64_t, const float*, int n_parts, int64_t part_rows,
+                              int64_t, const float*, const int32_t* row_map, uint16_t* const out[2],
+                              float* const out32[2], hipStream_t) {
   if (fail_now()) return hipErrorLaunchFailure;
   if (n_tensors < 1 || rows < 0 || n_parts < 0) err("reduce: arguments");
+  for (int t = 0; t < n_tensors; ++t)
+    if (!out[t] && !out32[t]) err("reduce: tensor without output");
+  const char* rm = reinterpret_cast<const char*>(row_map);
+  if (row_map && g_ws && rm >= g_ws && rm + (size_t)n_parts * rows * 4 <= g_ws + g_ws_bytes) {
+    // a map the library built: every row has its first term, and the mapped
+    // source rows are exactly the slab rows the dK/dV tiles wrote, each once
+    std::vector<int> used(part_rows, 0);
+    for (int64_t r = 0; r < rows; ++r) {
+      if (row_map[r] < 0) err("reduce: row without a first term");
+      for (int k = 0; k < n_parts; ++k) {
+        const int32_t v = row_map[(int64_t)k * rows + r];
+        if (v < -1 || v >= part_rows) {
+          err("reduce: source row out of range");
+          return hipSuccess;
+        }
+        if (v >= 0) used[v] += 1;
+      }
+    }
+    for (int64_t v = 0; v < part_rows; ++v) {
+      const int w = v < (int64_t)g_slab.size() ? g_slab[v] : 0;
+      if (used[v] != 1 || w != 1) {
+        err("reduce: slab row " + std::to_string(v) + " mapped " + std::to_string(used[v]) + " times, written " +
+            std::to_string(w) + " times");
+        break;
+      }
+    }
+    cover("dk_p", rows, 0, rows);
+  }
   g_counts.launches++;
   return hipSuccess;
 }

@@ -23,3 +23,7 @@ const FakeCounts& fake_counts();
 const std::vector<std::string>& fake_errors();
 void fake_check_coverage(const char* name, int64_t rows);
 void fake_reset_coverage();
+// the workspace of the call under test: row maps inside it are checked
+void fake_set_workspace(const void* ws, size_t bytes);
+// per fp32 slab row: how many dK/dV tiles wrote it
+const std::vector<int>& fake_slab_rows();

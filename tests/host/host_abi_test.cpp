@@ -19,6 +19,7 @@
 namespace {
 
 int g_fail = 0;
+int g_chunked = 0;  // chunked tree backward schedules checked
 #define CHECK(c, ...)                                              \
   do {                                                             \
     if (!(c)) {                                                    \
@@ -93,6 +94,34 @@ void expect_clean(const char* what) {
   for (const auto& e : fake_errors()) CHECK(false, "%s: %s", what, e.c_str());
 }
 
+// the fp32 slab rows written by the dK/dV tiles: [start, start + len) for each
+// start, each exactly once, and no other row
+void expect_slab(const char* what, const std::vector<int64_t>& starts, int64_t len) {
+  const std::vector<int>& w = fake_slab_rows();
+  std::vector<int> want(w.size(), 0);
+  for (int64_t st : starts)
+    for (int64_t r = st; r < st + len; ++r) {
+      if (r >= (int64_t)want.size()) want.resize(r + 1, 0);
+      want[r] += 1;
+    }
+  bool same = true;
+  for (size_t r = 0; r < std::max(w.size(), want.size()); ++r) {
+    const int a = r < w.size() ? w[r] : 0, b = r < want.size() ? want[r] : 0;
+    if (a != b || b > 1) same = false;
+  }
+  CHECK(same, "%s: fp32 slab rows", what);
+}
+
+// slab rows of the chunked tree backward: sum over groups of chunks x P
+int64_t chunk_slab_rows(const Batch& b) {
+  int64_t v = 0;
+  for (size_t g = 0; g + 1 < b.cp.size(); ++g) {
+    const int64_t nr = b.cr[b.cb[g + 1]] - b.cr[b.cb[g]];
+    v += (int64_t)augtree::tree_chunk_count(nr, b.hq / b.hkv) * (b.cp[g + 1] - b.cp[g]);
+  }
+  return v;
+}
+
 using u16 = uint16_t;
 
 int call(const Batch& b, int which, Ws& ws, int arg) {
@@ -121,15 +150,20 @@ const int kOp[6] = {AUGTREE_OP_PREFILL_FWD, AUGTREE_OP_REPLAY_FWD, AUGTREE_OP_PR
 
 void check_batch(const Batch& b) {
   const int64_t tp = b.tp(), tr = b.tr();
-  struct Case { int which, arg; };
-  const Case cases[] = {{0, 0}, {1, AUGTREE_REPLAY_FUSED}, {1, AUGTREE_REPLAY_SPLIT}, {1, AUGTREE_REPLAY_AUTO},
-                        {2, 0}, {3, 1}, {3, 2}, {3, 3}, {4, AUGTREE_REPLAY_FUSED}, {4, AUGTREE_REPLAY_AUTO},
-                        {5, 0}, {5, 1}};
+  // chunk: the tree backward's chunk setting (0: the default; 3: chunks of
+  // at most 3 query blocks, i.e. nearly every group chunked)
+  struct Case { int which, arg, chunk; };
+  const Case cases[] = {{0, 0, 0}, {1, AUGTREE_REPLAY_FUSED, 0}, {1, AUGTREE_REPLAY_SPLIT, 0},
+                        {1, AUGTREE_REPLAY_AUTO, 0}, {2, 0, 0}, {3, 1, 0}, {3, 2, 0}, {3, 3, 0},
+                        {4, AUGTREE_REPLAY_FUSED, 0}, {4, AUGTREE_REPLAY_AUTO, 0}, {5, 0, 0}, {5, 1, 0},
+                        {5, 0, 3}, {5, 1, 3}};
   for (const Case& c : cases) {
+    CHECK(augtree_set_tree_chunk_blocks(c.chunk) == AUGTREE_OK, "chunk setting");
     const size_t need = augtree_workspace_size(&b.g, kOp[c.which], c.which == 5 ? 0 : c.arg);
     CHECK(need > 0 && need % 256 == 0, "workspace size %zu", need);
     Ws ws(need);
     fake_set_shape(shape_of(b));
+    fake_set_workspace(ws.p, ws.n);
     fake_fail_at(0);
     const int st = call(b, c.which, ws, c.arg);
     CHECK(st == AUGTREE_OK, "entry %d arg %d: status %d (%s)", c.which, c.arg, st, augtree_last_error());
@@ -153,13 +187,17 @@ void check_batch(const Batch& b) {
       case 2:
         CHECK(n.dq_pairs == b.prefill && n.dkv_pairs == b.prefill, "prefill bwd pairs");
         fake_check_coverage("dq_p", tp);
-        fake_check_coverage("slab0", tp);
+        expect_slab("prefill bwd", {0}, tp);
         break;
       case 3:
         CHECK(n.dq_pairs == b.rp + b.rr && n.dkv_pairs == b.rp + b.rr, "replay bwd pairs (n_seed %d)", c.arg);
         fake_check_coverage("dq_r", tr);
         fake_check_coverage("dk_r", tr);
-        for (int k = 0; k < c.arg; ++k) fake_check_coverage(("slab" + std::to_string(k)).c_str(), tp);
+        {
+          std::vector<int64_t> st;
+          for (int k = 0; k < c.arg; ++k) st.push_back(2 * k * tp);
+          expect_slab("replay bwd", st, tp);
+        }
         break;
       case 4:
         CHECK(n.fwd_pairs == b.prefill + b.rp + b.rr, "tree fwd pairs");
@@ -172,7 +210,15 @@ void check_batch(const Batch& b) {
         fake_check_coverage("dq_r", tr);
         fake_check_coverage("dk_p", tp);
         fake_check_coverage("dk_r", tr);
-        if (c.arg) fake_check_coverage("slab0", tp);
+        {
+          const int64_t v = chunk_slab_rows(b);
+          if (v > tp) {  // then the reduce checked its row map
+            expect_slab("tree bwd chunks", {0}, v);
+            ++g_chunked;
+          }
+          else if (c.arg) expect_slab("tree bwd fp32 copy", {0}, tp);
+          else expect_slab("tree bwd", {}, 0);
+        }
         break;
     }
     // every launch and copy of the call failing in turn: AUGTREE_ERR_HIP, a message, no crash
@@ -187,6 +233,7 @@ void check_batch(const Batch& b) {
       CHECK(std::strlen(augtree_last_error()) > 0, "injected failure %d: no message", k);
     }
   }
+  augtree_set_tree_chunk_blocks(0);
 }
 
 int fake_scratch_ok(void** ws) {
@@ -236,6 +283,23 @@ void check_errors() {
   fake_set_shape(shape_of(b));
   CHECK(run_impl(fake_scratch_ok, 1 << 22) == AUGTREE_OK, "scratch run: %s", augtree_last_error());
   expect_clean("scratch schedule");
+  // chunk setting: negative rejected, 0 restores the default
+  CHECK(augtree_set_tree_chunk_blocks(-1) == AUGTREE_ERR_INVALID_ARGUMENT, "negative chunk blocks");
+  CHECK(augtree_set_tree_chunk_blocks(5) == AUGTREE_OK && augtree_tree_chunk_blocks() == 5, "chunk blocks set");
+  // with chunks whose slab does not fit, the allocation-free path runs the
+  // unchunked schedule (and checks against its size)
+  CHECK(augtree_set_tree_chunk_blocks(1) == AUGTREE_OK, "chunk blocks set");
+  const size_t chunked = augtree_workspace_size(&b.g, AUGTREE_OP_TREE_BWD, 0);
+  CHECK(augtree_set_tree_chunk_blocks(1 << 30) == AUGTREE_OK, "chunk blocks set");
+  const size_t plain = augtree_workspace_size(&b.g, AUGTREE_OP_TREE_BWD, 0);
+  CHECK(chunked > plain, "chunked workspace %zu vs %zu", chunked, plain);
+  CHECK(augtree_set_tree_chunk_blocks(1) == AUGTREE_OK, "chunk blocks set");
+  fake_set_shape(shape_of(b));
+  CHECK(run_impl(fake_scratch_ok, plain) == AUGTREE_OK, "scratch fallback: %s", augtree_last_error());
+  expect_clean("scratch fallback schedule");
+  expect_slab("scratch fallback", {}, 0);
+  CHECK(run_impl(fake_scratch_ok, plain - 1) == AUGTREE_ERR_WORKSPACE, "scratch fallback size check");
+  CHECK(augtree_set_tree_chunk_blocks(0) == AUGTREE_OK && augtree_tree_chunk_blocks() == 2048, "default");
 }
 
 }  // namespace
@@ -267,6 +331,6 @@ int main() {
     std::printf("%d failures\n", g_fail);
     return 1;
   }
-  std::printf("ok (%zu batches)\n", batches.size());
+  std::printf("ok (%zu batches, %d chunked tree backward schedules)\n", batches.size(), g_chunked);
   return 0;
 }

@@ -73,3 +73,52 @@ def test_tree_bwd_rejects_bad_arguments():
     lib = api._lib.load()
     st = lib.augtree_tree_bwd(b.ref, *([None] * 19), None, 0, None)
     assert st == 1 and "null pointer" in lib.augtree_last_error().decode()
+
+
+@pytest.mark.parametrize("case", [0, 2, 3])
+def test_tree_chunked_prompt_sweeps(case):
+    """Prompt-key sweeps cut into chunks (3 query blocks each here, so every
+    group with more than 3 x 64 / g branch rows is chunked): dQ and the
+    branch-key gradients are bitwise those of the six separate calls, the
+    prompt-key gradient agrees with the six-call and the unchunked sums to
+    fp32 rounding, and its bf16 output is its fp32 value rounded once."""
+    ps, rs, hq, hkv, d, mode = CASES[case]
+    shape = I.custom_shape(ps, rs, hq, hkv, d)
+    gi = I.make_inputs(shape, seed=700 + case, qk_mult=1.0)
+    b = GroupBatch.from_shape(shape)
+    x = upload(gi)
+    plain = SharedStep(b, "cuda", mode=mode, path="tree")
+    plain.run(x)
+    f32_plain = api.tree_bwd(b, x["q_p"], x["k_p"], x["v_p"], plain.o_p, plain.lse_p, x["do_p"], x["q_r"],
+                             x["k_r"], x["v_r"], plain.o_r, plain.lse_r, x["do_r"], want_f32=True)[6]
+    api.set_tree_chunk_blocks(3)
+    try:
+        tree = SharedStep(b, "cuda", mode=mode, path="tree")
+        tree.run(x)
+        f32 = api.tree_bwd(b, x["q_p"], x["k_p"], x["v_p"], tree.o_p, tree.lse_p, x["do_p"], x["q_r"], x["k_r"],
+                           x["v_r"], tree.o_r, tree.lse_r, x["do_r"], want_f32=True)[6]
+    finally:
+        api.set_tree_chunk_blocks(0)
+    calls = SharedStep(b, "cuda", mode=mode, n_seed=1, path="calls")
+    calls.run(x)
+    _, calls_f32 = api.prompt_grad_reduce(calls.seed, self_part=calls.dkv_self, want_bf16=False)
+    torch.cuda.synchronize()
+    a = {k: v.clone() for k, v in tree.outputs().items()}
+    c = calls.outputs()
+    for k in ("o_p", "lse_p", "o_r", "lse_r", "dq_p", "dq_r", "dk_r", "dv_r"):
+        assert torch.equal(a[k].contiguous().view(torch.uint8), c[k].contiguous().view(torch.uint8)), k
+    e_calls = rel(f32.double().cpu().numpy(), calls_f32.double().cpu().numpy())
+    e_plain = rel(f32.double().cpu().numpy(), f32_plain.double().cpu().numpy())
+    log(f"[tree chunks] case {case}: prompt dK/dV fp32 rel diff vs calls {e_calls:.2e}, vs unchunked {e_plain:.2e}")
+    assert e_calls < 1e-5 and e_plain < 1e-5
+    assert torch.equal(f32[0].to(torch.bfloat16), a["dk_p"]) and torch.equal(f32[1].to(torch.bfloat16), a["dv_p"])
+    # a second run gives the same bits
+    api.set_tree_chunk_blocks(3)
+    try:
+        tree.run(x)
+    finally:
+        api.set_tree_chunk_blocks(0)
+    torch.cuda.synchronize()
+    a2 = tree.outputs()
+    for k in ("dk_p", "dv_p", "dq_p", "dq_r"):
+        assert torch.equal(a[k].view(torch.uint8), a2[k].view(torch.uint8)), k

@@ -35,3 +35,5 @@ def test_host_logic_under_sanitizers(tmp_path):
     env = dict(os.environ, ASAN_OPTIONS="detect_leaks=1:verify_asan_link_order=0", UBSAN_OPTIONS="print_stacktrace=1")
     r = subprocess.run([exe], capture_output=True, text=True, env=env, timeout=500)
     assert r.returncode == 0 and r.stdout.startswith("ok"), (r.stdout[-4000:] + r.stderr[-4000:])
+    chunked = int(r.stdout.split(",")[1].split()[0])
+    assert chunked >= 40, r.stdout   # the chunked tree backward was exercised
