@@ -84,7 +84,7 @@ def tree_chunk_rows(shape, chunk_blocks: int) -> int:
     return sum(c * p for c, p in zip(n, shape.prompt_lens))
 
 
-def role_work(role: str, shape, n_seed: int, split=None, chunk_blocks: int = 2048):
+def role_work(role: str, shape, n_seed: int, split=None, chunk_blocks: int = 1024):
     """Algorithmic work of one step's launches of a role: ('flop', F) for
     contractions, ('byte', B) for the HBM-bound kernels. `split` flags the
     groups whose replay forward runs SPLIT (None: none of them)."""
@@ -612,6 +612,8 @@ def main():
     ap.add_argument("--path", default="tree", choices=("tree", "calls"),
                     help="tree: augtree_tree_fwd + augtree_tree_bwd; calls: the six separate entry points")
     ap.add_argument("--n-seed", type=int, default=None, help="prompt-key chunks of the six-call path")
+    ap.add_argument("--chunk-blocks", type=int, default=0,
+                    help="tree backward: query blocks per prompt-key sweep before it is chunked (0: the default)")
     ap.add_argument("--no-flattened", action="store_true")
     ap.add_argument("--no-cpu", action="store_true")
     ap.add_argument("--no-per-config", action="store_true")
@@ -660,6 +662,7 @@ def main():
         print("bench.py needs an MI355X (gfx950): " + lib.augtree_last_error().decode(), file=sys.stderr)
         sys.exit(3)
     torch.cuda.set_device(0)
+    api.set_tree_chunk_blocks(args.chunk_blocks)
     if args.copy_calibration:
         src = torch.ones(1 << 28, dtype=torch.float32, device="cuda:0")
         dst = torch.empty_like(src)
@@ -805,6 +808,7 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "config": {"workload": WORKLOAD_TEXT[args.workload], "replay_mode": args.mode, "path": args.path,
                    "n_seed": n_seed if args.path == "calls" else None,
+                   "tree_chunk_blocks": api.tree_chunk_blocks() if args.path == "tree" else None,
                    "counted_tflop_per_step": round(counted / 1e12, 4), "flop_convention": "14*d*Hq*valid_pairs"},
         "pct_peak": round(100 * tflops / PEAK_BF16_TFLOPS, 2),
         "peak": {"bf16_dense_tflops_used": PEAK_BF16_TFLOPS, "source": "MI355X published dense bf16 MFMA peak",

@@ -360,7 +360,7 @@ void augtree_set_launch_hook(augtree_launch_hook hook, void* user);
  * computed after the call use it): the most query blocks (64 rows x one
  * query head) one prompt-key tile sweeps over a group's branch rows before
  * the sweep is cut into chunks. blocks >= 1 sets it, 0 restores the default
- * (2048); negative: AUGTREE_ERR_INVALID_ARGUMENT.
+ * (1024); negative: AUGTREE_ERR_INVALID_ARGUMENT.
  */
 int augtree_set_tree_chunk_blocks(int32_t blocks);
 int32_t augtree_tree_chunk_blocks(void);

@@ -29,7 +29,7 @@ int fail_status(int status, const char* msg);
 // Chunks of the tree backward's prompt-key sweep over a group's `nr` branch
 // rows (each chunk at most augtree_set_tree_chunk_blocks query blocks of 64
 // rows x one of the `group` query heads; between 1 and 64).
-constexpr int kTreeChunkBlocksDefault = 2048;
+constexpr int kTreeChunkBlocksDefault = 1024;
 int tree_chunk_count(int64_t nr, int group);
 
 }  // namespace augtree

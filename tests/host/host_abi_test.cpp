@@ -299,7 +299,7 @@ void check_errors() {
   expect_clean("scratch fallback schedule");
   expect_slab("scratch fallback", {}, 0);
   CHECK(run_impl(fake_scratch_ok, plain - 1) == AUGTREE_ERR_WORKSPACE, "scratch fallback size check");
-  CHECK(augtree_set_tree_chunk_blocks(0) == AUGTREE_OK && augtree_tree_chunk_blocks() == 2048, "default");
+  CHECK(augtree_set_tree_chunk_blocks(0) == AUGTREE_OK && augtree_tree_chunk_blocks() == 1024, "default");
 }
 
 }  // namespace
