@@ -11,8 +11,9 @@
  *
  * The library splits it the way the method does (§3.2, §3.3):
  *   prefill_fwd   causal attention over the prompt, run once per tree;
- *   replay_fwd    every branch against the stationary prompt KV plus its own
- *                 causal KV, two partial softmax states merged by log-sum-exp;
+ *   replay_fwd    every branch against the prompt KV (read in place, never
+ *                 copied) plus its own causal KV, two partial softmax states
+ *                 merged by log-sum-exp;
  *   lse_merge     the merge of partial states on its own;
  *   replay_bwd    gradients of the replay, with each branch's prompt-KV
  *                 gradient ("seed") accumulated on the prompt KV (Eq. 2);
@@ -231,7 +232,7 @@ int augtree_prefill_bwd(const augtree_groups* grp, const uint16_t* q_p, const ui
 
 /*
  * One tree step's forward in one call (§3.2: prefill once, then replay every
- * branch against the stationary prompt KV; Eq. 1; §3.3). Computes exactly what
+ * branch against the prompt KV read in place; Eq. 1; §3.3). Computes exactly what
  * augtree_prefill_fwd followed by augtree_replay_fwd compute (bit for bit:
  * the same kernels and per-row arithmetic), but the prefill tiles and the
  * fused replay tiles run in ONE kernel launch (fewer launches and one launch

@@ -5,7 +5,7 @@
 Inputs are the packed bf16 tensors of a batch of replay trees (prompt rows
 [T_P, H, d], response rows [T_R, H, d], `batch` the GroupBatch holding their
 offsets). Forward: augtree_tree_fwd (the prompt, causal, once per tree, and
-every branch against the stationary prompt KV plus its own causal KV; §3.2,
+every branch against the prompt KV, read in place, plus its own causal KV; §3.2,
 Eq. 1). Backward: augtree_tree_bwd (branch gradients, and the prompt-KV
 gradient of every branch plus the prompt queries' own contribution summed on
 the prompt KV in a fixed order, Eq. 2). Every step runs in the library's

@@ -2,7 +2,7 @@
 and the flattened per-branch baseline built from the same kernels.
 
 SharedStep (the method, §3.2-§3.3): the prompt prefilled once per tree, every
-branch replayed against the stationary prompt KV plus its own causal KV, the
+branch replayed against the prompt KV (read in place) plus its own causal KV, the
 branch gradients with every branch's prompt-KV gradient accumulated on the
 prompt KV (Eq. 2) together with the prompt queries' own contribution. By
 default as augtree_tree_fwd + augtree_tree_bwd; ``path="calls"`` strings the
