@@ -184,13 +184,16 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
       __builtin_amdgcn_sched_group_barrier(0x402, FWD_VALU_PER_MFMA, 0);
     }
     set_wave_priority<1>();
+    // k-step outer, output column block inner: consecutive MFMAs go to
+    // different accumulators (each still sums its four k-steps in order)
 #pragma unroll
-    for (int db = 0; db < D / 32; ++db) {
-      oacc[db] = mfma32(vtr_off.read(vl, 0, db), pb0, oacc[db]);
-      oacc[db] = mfma32(vtr_off.read(vl, 1, db), pb1, oacc[db]);
-      oacc[db] = mfma32(vtr_off.read(vl, 2, db), pb2, oacc[db]);
-      oacc[db] = mfma32(vtr_off.read(vl, 3, db), pb3, oacc[db]);
-    }
+    for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(vtr_off.read(vl, 0, db), pb0, oacc[db]);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(vtr_off.read(vl, 1, db), pb1, oacc[db]);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(vtr_off.read(vl, 2, db), pb2, oacc[db]);
+#pragma unroll
+    for (int db = 0; db < D / 32; ++db) oacc[db] = mfma32(vtr_off.read(vl, 3, db), pb3, oacc[db]);
     pace_lds_mfma<D / 8, 2, PV_DEPTH>();
     set_wave_priority<0>();
   };
