@@ -302,7 +302,11 @@ int augtree_tree_bwd(const augtree_groups* grp, const uint16_t* q_p, const uint1
  * exceeds it is rejected with AUGTREE_ERR_WORKSPACE before anything is
  * enqueued. Calls that overlap on
  * one GPU (several streams or threads) share the array and race; serialise
- * them.
+ * them. Stream capture: a launch whose tile schedule has more than 32 tiles
+ * (and a chunked batch's row map) receives it by a host-to-device copy from
+ * a host buffer the call frees on return, so a graph captured around such a
+ * call must not be replayed; batches of at most 32 tiles per launch and no
+ * chunks enqueue kernels only (schedules in the kernel arguments).
  */
 int augtree_tree_bwd_noalloc(const augtree_groups* grp, const uint16_t* q_p, const uint16_t* k_p,
                              const uint16_t* v_p, const uint16_t* o_p, const float* lse_p,
