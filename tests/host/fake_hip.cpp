@@ -200,7 +200,9 @@ hipError_t launch_attn_dkv(const DkvParams& p, int n_tiles, hipStream_t) {
       cover(pk ? "dk_p" : "dk_r", rows, t.kv_row0, t.kv_len);
     }
     if (t.flags & KV_OUT_SLAB) {
-      if (!p.slab || !pk || t.out_row0 < 0 || t.out_row0 + t.kv_len > p.slab_rows * 64) err("dkv: slab output");
+      // dK rows must leave room for the dV rows slab_rows further on; the
+      // seed layout [part][2][T_P] reaches 2 x 64 x T_P rows
+      if (!p.slab || !pk || t.out_row0 < 0 || t.out_row0 + t.kv_len > p.slab_rows * 128) err("dkv: slab output");
       if ((int64_t)g_slab.size() < (int64_t)t.out_row0 + t.kv_len) g_slab.resize(t.out_row0 + t.kv_len, 0);
       for (int j = 0; j < t.kv_len; ++j) g_slab[t.out_row0 + j] += 1;
     }

@@ -154,7 +154,7 @@ void check_batch(const Batch& b) {
   // at most 3 query blocks, i.e. nearly every group chunked)
   struct Case { int which, arg, chunk; };
   const Case cases[] = {{0, 0, 0}, {1, AUGTREE_REPLAY_FUSED, 0}, {1, AUGTREE_REPLAY_SPLIT, 0},
-                        {1, AUGTREE_REPLAY_AUTO, 0}, {2, 0, 0}, {3, 1, 0}, {3, 2, 0}, {3, 3, 0},
+                        {1, AUGTREE_REPLAY_AUTO, 0}, {2, 0, 0}, {3, 1, 0}, {3, 2, 0}, {3, 3, 0}, {3, 64, 0},
                         {4, AUGTREE_REPLAY_FUSED, 0}, {4, AUGTREE_REPLAY_AUTO, 0}, {5, 0, 0}, {5, 1, 0},
                         {5, 0, 3}, {5, 1, 3}};
   for (const Case& c : cases) {
