@@ -3,12 +3,12 @@
 Notation follows the paper: a replay tree T = (P, {R_i}) has one prompt P and G
 response branches R_i (§2.1, §3.1). For one head, attention is
 O = softmax(Q K^T / sqrt(D_h) + M) V (§2.2). A token of branch i sees the whole
-prompt and its own prefix, never a sibling branch (§2.2 "replay mismatch";
-Eq. 1, KV(R_{i,t}) = KV_P ∪ KV(R_{i,<t})). Positions here are input positions:
+prompt and its own prefix, never a sibling branch (§2.2; Eq. 1,
+KV(R_{i,t}) = KV_P ∪ KV(R_{i,<t})). Positions here are input positions:
 query row r sees keys j <= r (the standard causal mask of the flattened
 sequence [P; R_i]).
 
-Conventions (readings of the paper, listed in the design doc):
+Conventions (readings of the paper where it leaves a choice):
 * LSE is the natural log of the sum of exp of the *scaled* logits over the
   visible keys; a row with no visible key has LSE = -inf and O = 0.
 * The partial softmax state of §3.3, (m, l, O_acc), is carried as
