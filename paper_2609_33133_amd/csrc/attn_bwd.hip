@@ -307,22 +307,30 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   const int nxblk = p.group * nxb;
   const int nblk = nxblk + p.group * nyb;
 
-  // Block b -> (range, query head, 64-row block). Inside a range the query
-  // blocks are swept from the end backwards and the g heads of a block are
-  // taken one after the other, so that the concurrent tiles of one KV head
-  // (causal ranges all end at the segment end; the response rows of a group
-  // are the same for all its prompt key tiles) stay at the same query rows
-  // and share the Q / dO blocks in L2.
+  // Query blocks in sweep order: (range, query head of the group, 64-row
+  // block). Inside a range the blocks are swept from the end backwards and
+  // the g heads of a block are taken one after the other, so that the
+  // concurrent tiles of one KV head (causal ranges all end at the segment end;
+  // the response rows of a group are the same for all its prompt key tiles)
+  // stay at the same query rows and share the Q / dO blocks in L2. The sweep
+  // steps from one block to the next with compares only (no division per
+  // block: the scalar unit is shared by the SIMDs of the CU).
   struct Blk {
-    int y, hh, qb;
+    int y, hl, qb;  // range (0: X, 1: Y), head within the group, block (counting down)
   };
-  auto block_of = [&](int b) -> Blk {
-    Blk r;
-    r.y = b >= nxblk;
-    const int bb = r.y ? b - nxblk : b;
-    const int nb = r.y ? nyb : nxb;
-    r.hh = kvh * p.group + bb % p.group;
-    r.qb = nb - 1 - bb / p.group;
+  const int g = p.group;
+  Blk first;
+  first.y = nxb > 0 ? 0 : 1;
+  first.hl = 0;
+  first.qb = (first.y ? nyb : nxb) - 1;
+  auto next_blk = [&](Blk r) -> Blk {
+    if (++r.hl == g) {
+      r.hl = 0;
+      if (--r.qb < 0 && r.y == 0) {
+        r.y = 1;
+        r.qb = nyb - 1;
+      }
+    }
     return r;
   };
 
@@ -341,14 +349,14 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   const uint16_t* const do_src[2] = {p.dout[0], p.dout[1]};
   const float* const st_src[2] = {wave_u == 0 ? p.lse[0] : p.dsum[0], wave_u == 0 ? p.lse[1] : p.dsum[1]};
   const int64_t st_rows[2] = {p.lse_rows[0], p.lse_rows[1]};
-  auto load_block = [&](int b, __bf16* qd, __bf16* od) {
-    const Blk k = block_of(b);
+  auto load_block = [&](const Blk& k, __bf16* qd, __bf16* od) {
+    const int hh = kvh * g + k.hl;
     const int64_t row0 = (int64_t)(k.y ? t.kv_row0 : t.x_row0) + k.qb * KV_BQ;
     const int nvalid = min(KV_BQ, (k.y ? t.y_len : t.x_len) - k.qb * KV_BQ);
-    qc.issue(qd, k.y ? q_src[1] : q_src[0], row0, nvalid, qstride, k.hh * D);
-    qc.issue(od, k.y ? do_src[1] : do_src[0], row0, nvalid, qstride, k.hh * D);
+    qc.issue(qd, k.y ? q_src[1] : q_src[0], row0, nvalid, qstride, hh * D);
+    qc.issue(od, k.y ? do_src[1] : do_src[0], row0, nvalid, qstride, hh * D);
     if (wave_u < 2) {
-      const float* src = (k.y ? st_src[1] : st_src[0]) + (int64_t)k.hh * (k.y ? st_rows[1] : st_rows[0]) + row0;
+      const float* src = (k.y ? st_src[1] : st_src[0]) + (int64_t)hh * (k.y ? st_rows[1] : st_rows[0]) + row0;
       stat = src[min(lane, nvalid - 1)];
       stat_n = nvalid;
     }
@@ -371,8 +379,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   for (int ks = 0; ks < D / 16; ++ks) key_off.o[ks] = (int)opaque(lds_addr(k_tile) + key_off.o[ks]);
   TrOffsets<D> qtr_off;              // Q^T / dO^T operands of this wave's half
   qtr_off.init(qs * 32, lane);
-  auto compute = [&](int b, const __bf16* ql, const __bf16* dl, const float* lsel, const float* dsl) {
-    const Blk k = block_of(b);
+  auto compute = [&](const Blk& k, const __bf16* ql, const __bf16* dl, const float* lsel, const float* dsl) {
     const bool causal = k.y || x_causal;
     const int qpos0 = t.kpos0 + k.qb * KV_BQ + qs * 32;  // position of this wave's first query (causal)
     const bool skip = causal && (qpos0 + 31 < t.kpos0 + kw0);
@@ -425,24 +432,28 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     set_wave_priority<1>();
   };
 
+  Blk cur = first;
   if (nblk > 0) {
-    load_block(0, q_buf0, o_buf0);
+    load_block(cur, q_buf0, o_buf0);
     store_stat(nlse_buf0, ndsum_buf0);
   }
   wait_vmem();
   __syncthreads();
   for (int b = 0; b < nblk; b += 2) {
-    if (b + 1 < nblk) load_block(b + 1, q_buf1, o_buf1);
-    compute(b, q_buf0, o_buf0, nlse_buf0, ndsum_buf0);
+    const Blk b1 = next_blk(cur);
+    if (b + 1 < nblk) load_block(b1, q_buf1, o_buf1);
+    compute(cur, q_buf0, o_buf0, nlse_buf0, ndsum_buf0);
     if (b + 1 < nblk) store_stat(nlse_buf1, ndsum_buf1);
     wait_vmem();
     __syncthreads();
     if (b + 1 < nblk) {
-      if (b + 2 < nblk) load_block(b + 2, q_buf0, o_buf0);
-      compute(b + 1, q_buf1, o_buf1, nlse_buf1, ndsum_buf1);
+      const Blk b2 = next_blk(b1);
+      if (b + 2 < nblk) load_block(b2, q_buf0, o_buf0);
+      compute(b1, q_buf1, o_buf1, nlse_buf1, ndsum_buf1);
       if (b + 2 < nblk) store_stat(nlse_buf0, ndsum_buf0);
       wait_vmem();
       __syncthreads();
+      cur = b2;
     }
   }
 
