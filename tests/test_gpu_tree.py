@@ -75,7 +75,7 @@ def test_tree_bwd_rejects_bad_arguments():
     assert st == 1 and "null pointer" in lib.augtree_last_error().decode()
 
 
-@pytest.mark.parametrize("case", [0, 2, 3])
+@pytest.mark.parametrize("case", [0, 1, 2, 3])
 def test_tree_chunked_prompt_sweeps(case):
     """Prompt-key sweeps cut into chunks (3 query blocks each here, so every
     group with more than 3 x 64 / g branch rows is chunked): dQ and the
