@@ -105,14 +105,20 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 
   TileCopy<DQ_BN, D, 4> cp;
   cp.init(kvstride);
+  // K / V of both segments at the segment's first row and this KV head, so
+  // that a block needs one offset
+  const uint16_t* const ka0 = p.ka + (int64_t)t.a_row0 * kvstride + kvh * D;
+  const uint16_t* const va0 = p.va + (int64_t)t.a_row0 * kvstride + kvh * D;
+  const uint16_t* const kb0p = kb + (int64_t)t.b_row0 * kvstride + kvh * D;
+  const uint16_t* const vb0p = vb + (int64_t)t.b_row0 * kvstride + kvh * D;
   auto load_block = [&](int b, __bf16* kd, __bf16* vd) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * DQ_BN;
     const int len = isB ? t.b_len : t.a_len;
-    const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
     const int nvalid = min(DQ_BN, len - kb0);
-    cp.issue(kd, isB ? kb : p.ka, row0, nvalid, kvstride, kvh * D);
-    cp.issue(vd, isB ? vb : p.va, row0, nvalid, kvstride, kvh * D);
+    const int64_t off = (int64_t)kb0 * kvstride;
+    cp.issue_at(kd, (isB ? kb0p : ka0) + off, nvalid, kvstride);
+    cp.issue_at(vd, (isB ? vb0p : va0) + off, nvalid, kvstride);
   };
 
   RowOffsets<D> r0_off, r1_off;  // K/V rows l32 and 32 + l32
@@ -344,19 +350,25 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   qc.init(qstride);
   // the query-side tensors of both ranges, read from the kernel arguments
   // once (a per-block indexed read of the arguments would be a scalar load
-  // plus a wait in the loop)
-  const uint16_t* const q_src[2] = {p.q[0], p.q[1]};
-  const uint16_t* const do_src[2] = {p.dout[0], p.dout[1]};
-  const float* const st_src[2] = {wave_u == 0 ? p.lse[0] : p.dsum[0], wave_u == 0 ? p.lse[1] : p.dsum[1]};
-  const int64_t st_rows[2] = {p.lse_rows[0], p.lse_rows[1]};
+  // plus a wait in the loop), at the range's first row and the KV head's
+  // first query head, so that a block needs one offset
+  const int64_t h0 = (int64_t)kvh * g;
+  const int64_t xr0 = t.x_row0, yr0 = t.kv_row0;
+  const uint16_t* const qx = p.q[0] + xr0 * qstride + h0 * D;
+  const uint16_t* const qy = p.q[1] + yr0 * qstride + h0 * D;
+  const uint16_t* const ox = p.dout[0] + xr0 * qstride + h0 * D;
+  const uint16_t* const oy = p.dout[1] + yr0 * qstride + h0 * D;
+  const int64_t srx = p.lse_rows[0], sry = p.lse_rows[1];
+  const float* const sx = (wave_u == 0 ? p.lse[0] : p.dsum[0]) + h0 * srx + xr0;
+  const float* const sy = (wave_u == 0 ? p.lse[1] : p.dsum[1]) + h0 * sry + yr0;
   auto load_block = [&](const Blk& k, __bf16* qd, __bf16* od) {
-    const int hh = kvh * g + k.hl;
-    const int64_t row0 = (int64_t)(k.y ? t.kv_row0 : t.x_row0) + k.qb * KV_BQ;
-    const int nvalid = min(KV_BQ, (k.y ? t.y_len : t.x_len) - k.qb * KV_BQ);
-    qc.issue(qd, k.y ? q_src[1] : q_src[0], row0, nvalid, qstride, hh * D);
-    qc.issue(od, k.y ? do_src[1] : do_src[0], row0, nvalid, qstride, hh * D);
+    const int r = k.qb * KV_BQ;  // the block's first row inside its range
+    const int nvalid = min(KV_BQ, (k.y ? t.y_len : t.x_len) - r);
+    const int64_t off = (int64_t)r * qstride + k.hl * D;
+    qc.issue_at(qd, (k.y ? qy : qx) + off, nvalid, qstride);
+    qc.issue_at(od, (k.y ? oy : ox) + off, nvalid, qstride);
     if (wave_u < 2) {
-      const float* src = (k.y ? st_src[1] : st_src[0]) + (int64_t)hh * (k.y ? st_rows[1] : st_rows[0]) + row0;
+      const float* src = (k.y ? sy : sx) + (int64_t)k.hl * (k.y ? sry : srx) + r;
       stat = src[min(lane, nvalid - 1)];
       stat_n = nvalid;
     }

@@ -219,11 +219,14 @@ struct TileCopy {
   // columns col0 .. col0 + D - 1; tile rows from nvalid on are zero
   __device__ __forceinline__ void issue(__bf16* lds, const uint16_t* base, int64_t row0, int nvalid, int64_t stride,
                                         int col0) const {
+    issue_at(lds, base + row0 * stride + col0, nvalid, stride);
+  }
+  // the same from the address of the first row's first column
+  __device__ __forceinline__ void issue_at(__bf16* lds, const uint16_t* gb, int nvalid, int64_t stride) const {
     // Device pass only: with a buffer-resource value in a kernel body, the
     // host pass silently drops the launch stubs of some instantiations.
 #if defined(__HIP_DEVICE_COMPILE__)
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const uint16_t* gb = base + row0 * stride + col0;
     const int rows = nvalid < ROWS ? nvalid : ROWS;
     const __amdgpu_buffer_rsrc_t rsrc =
         __builtin_amdgcn_make_buffer_rsrc((void*)gb, 0, (int)(rows * stride * 2), 0x00020000);
