@@ -86,13 +86,18 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
   TileCopy<BN, D, 4> cp;
   cp.init(kvstride);
+  // K / V of both segments at the segment's first row and this KV head, so
+  // that a block needs one offset
+  const uint16_t* const ka0 = p.ka + (int64_t)t.a_row0 * kvstride + kvh * D;
+  const uint16_t* const va0 = p.va + (int64_t)t.a_row0 * kvstride + kvh * D;
+  const uint16_t* const kb0p = kb + (int64_t)t.b_row0 * kvstride + kvh * D;
+  const uint16_t* const vb0p = vb + (int64_t)t.b_row0 * kvstride + kvh * D;
   auto load = [&](int b, bool val, __bf16* dst) {
     const bool isB = b >= nA;
     const int kb0 = (isB ? b - nA : b) * BN;
     const int len = isB ? t.b_len : t.a_len;
-    const int64_t row0 = (int64_t)(isB ? t.b_row0 : t.a_row0) + kb0;
-    const uint16_t* src = val ? (isB ? vb : p.va) : (isB ? kb : p.ka);
-    cp.issue(dst, src, row0, min(BN, len - kb0), kvstride, kvh * D);
+    const uint16_t* src = val ? (isB ? vb0p : va0) : (isB ? kb0p : ka0);
+    cp.issue_at(dst, src + (int64_t)kb0 * kvstride, min(BN, len - kb0), kvstride);
   };
 
   RowOffsets<D> k_off;  // K row l32; row 32 + l32 has the same swizzle, 32 rows further
