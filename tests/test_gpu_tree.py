@@ -75,13 +75,15 @@ def test_tree_bwd_rejects_bad_arguments():
     assert st == 1 and "null pointer" in lib.augtree_last_error().decode()
 
 
-@pytest.mark.parametrize("case", [0, 1, 2, 3])
-def test_tree_chunked_prompt_sweeps(case):
-    """Prompt-key sweeps cut into chunks (3 query blocks each here, so every
-    group with more than 3 x 64 / g branch rows is chunked): dQ and the
-    branch-key gradients are bitwise those of the six separate calls, the
-    prompt-key gradient agrees with the six-call and the unchunked sums to
-    fp32 rounding, and its bf16 output is its fp32 value rounded once."""
+@pytest.mark.parametrize("case,chunk", [(0, 3), (1, 3), (2, 3), (3, 3), (0, 1)])
+def test_tree_chunked_prompt_sweeps(case, chunk):
+    """Prompt-key sweeps cut into chunks (3 query blocks each, so every group
+    with more than 3 x 64 / g branch rows is chunked; with 1 block the chunk
+    edges round to 64-row multiples and many chunks are empty, their partials
+    zero): dQ and the branch-key gradients are bitwise those of the six
+    separate calls, the prompt-key gradient agrees with the six-call and the
+    unchunked sums to fp32 rounding, and its bf16 output is its fp32 value
+    rounded once."""
     ps, rs, hq, hkv, d, mode = CASES[case]
     shape = I.custom_shape(ps, rs, hq, hkv, d)
     gi = I.make_inputs(shape, seed=700 + case, qk_mult=1.0)
@@ -91,7 +93,7 @@ def test_tree_chunked_prompt_sweeps(case):
     plain.run(x)
     f32_plain = api.tree_bwd(b, x["q_p"], x["k_p"], x["v_p"], plain.o_p, plain.lse_p, x["do_p"], x["q_r"],
                              x["k_r"], x["v_r"], plain.o_r, plain.lse_r, x["do_r"], want_f32=True)[6]
-    api.set_tree_chunk_blocks(3)
+    api.set_tree_chunk_blocks(chunk)
     try:
         tree = SharedStep(b, "cuda", mode=mode, path="tree")
         tree.run(x)
@@ -109,11 +111,12 @@ def test_tree_chunked_prompt_sweeps(case):
         assert torch.equal(a[k].contiguous().view(torch.uint8), c[k].contiguous().view(torch.uint8)), k
     e_calls = rel(f32.double().cpu().numpy(), calls_f32.double().cpu().numpy())
     e_plain = rel(f32.double().cpu().numpy(), f32_plain.double().cpu().numpy())
-    log(f"[tree chunks] case {case}: prompt dK/dV fp32 rel diff vs calls {e_calls:.2e}, vs unchunked {e_plain:.2e}")
+    log(f"[tree chunks] case {case} chunk {chunk}: prompt dK/dV fp32 rel diff vs calls {e_calls:.2e}, "
+        f"vs unchunked {e_plain:.2e}")
     assert e_calls < 1e-5 and e_plain < 1e-5
     assert torch.equal(f32[0].to(torch.bfloat16), a["dk_p"]) and torch.equal(f32[1].to(torch.bfloat16), a["dv_p"])
     # a second run gives the same bits
-    api.set_tree_chunk_blocks(3)
+    api.set_tree_chunk_blocks(chunk)
     try:
         tree.run(x)
     finally:
