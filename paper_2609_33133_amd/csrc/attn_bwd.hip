@@ -105,20 +105,48 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
 
   TileCopy<DQ_BN, D, 4> cp;
   cp.init(kvstride);
-  // K / V of both segments at the segment's first row and this KV head, so
-  // that a block needs one offset
-  const uint16_t* const ka0 = p.ka + (int64_t)t.a_row0 * kvstride + kvh * D;
-  const uint16_t* const va0 = p.va + (int64_t)t.a_row0 * kvstride + kvh * D;
-  const uint16_t* const kb0p = kb + (int64_t)t.b_row0 * kvstride + kvh * D;
-  const uint16_t* const vb0p = vb + (int64_t)t.b_row0 * kvstride + kvh * D;
-  auto load_block = [&](int b, __bf16* kd, __bf16* vd) {
-    const bool isB = b >= nA;
-    const int kb0 = (isB ? b - nA : b) * DQ_BN;
-    const int len = isB ? t.b_len : t.a_len;
-    const int nvalid = min(DQ_BN, len - kb0);
-    const int64_t off = (int64_t)kb0 * kvstride;
-    cp.issue_at(kd, (isB ? kb0p : ka0) + off, nvalid, kvstride);
-    cp.issue_at(vd, (isB ? vb0p : va0) + off, nvalid, kvstride);
+  // The load cursor: the next key block to be copied into LDS, stepped in
+  // place (the sweep's scalar work is on the critical path of every block:
+  // the eight wavefronts of a CU share one scalar unit).
+  struct KCursor {
+    int isB, kb0, len;    // segment (0: A, 1: B), its first key of the block, the segment's length
+    const char* kp;       // K of the block's first key, KV head kvh
+    const char* vp;       // V, the same
+  };
+  const int krow_bytes = (int)(kvstride * 2);
+  const int64_t kstep = (int64_t)DQ_BN * krow_bytes;
+  // K / V of segment B at its first row and this KV head
+  const char* const kb0p = reinterpret_cast<const char*>(kb + (int64_t)t.b_row0 * kvstride + kvh * D);
+  const char* const vb0p = reinterpret_cast<const char*>(vb + (int64_t)t.b_row0 * kvstride + kvh * D);
+  KCursor kc;
+  if (nA > 0) {
+    kc = {0, 0, t.a_len, reinterpret_cast<const char*>(p.ka + (int64_t)t.a_row0 * kvstride + kvh * D),
+          reinterpret_cast<const char*>(p.va + (int64_t)t.a_row0 * kvstride + kvh * D)};
+  } else {
+    kc = {1, 0, t.b_len, kb0p, vb0p};
+  }
+  // what the computation of a block needs to know of it
+  struct Blk {
+    int isB, kb0, len;
+  };
+  // copy the cursor's block into (kd, vd), note it in k and step the cursor
+  // (past the end of segment B: never loaded)
+  auto load_next = [&](__bf16* kd, __bf16* vd, Blk& k) {
+    const int nbytes = min(DQ_BN, kc.len - kc.kb0) * krow_bytes;
+    cp.issue_bytes(kd, reinterpret_cast<const uint16_t*>(kc.kp), nbytes);
+    cp.issue_bytes(vd, reinterpret_cast<const uint16_t*>(kc.vp), nbytes);
+    k = {kc.isB, kc.kb0, kc.len};
+    int64_t dk = kstep, dv = kstep;
+    kc.kb0 += DQ_BN;
+    if (kc.kb0 >= kc.len && kc.isB == 0) {
+      dk = kb0p - kc.kp;
+      dv = vb0p - kc.vp;
+      kc.isB = 1;
+      kc.kb0 = 0;
+      kc.len = t.b_len;
+    }
+    kc.kp += dk;
+    kc.vp += dv;
   };
 
   RowOffsets<D> r0_off, r1_off;  // K/V rows l32 and 32 + l32
@@ -126,10 +154,10 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
   r1_off.init(32 + l32, hf);
   TrOffsets<D> ktr_off;           // K^T operands
   ktr_off.init(0, lane);
-  auto compute = [&](int b, const __bf16* kl, const __bf16* vl) {
-    const bool isB = b >= nA;
-    const int kb0 = (isB ? b - nA : b) * DQ_BN;
-    const int len = isB ? t.b_len : t.a_len;
+  auto compute = [&](const Blk& k, const __bf16* kl, const __bf16* vl) {
+    const bool isB = k.isB != 0;
+    const int kb0 = k.kb0;
+    const int len = k.len;
     const int qpos_lo = t.b_qpos + wave * 32;
     const int qpos = t.b_qpos + qi;
 #pragma unroll
@@ -173,7 +201,8 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
     }
   };
 
-  if (nblk > 0) load_block(0, k_buf0, v_buf0);
+  Blk c0{0, 0, 0}, c1{0, 0, 0};
+  if (nblk > 0) load_next(k_buf0, v_buf0, c0);
   wait_vmem();
   __syncthreads();
   // The vector c of the common-mode correction at the end: the mean of the
@@ -205,13 +234,13 @@ __global__ __launch_bounds__(256, 2) void attn_dq_kernel(DqParams p) {
       for (int e = 0; e < 8; ++e) kmean_part[wave][ch * 8 + e] = part[e];
   }
   for (int b = 0; b < nblk; b += 2) {
-    if (b + 1 < nblk) load_block(b + 1, k_buf1, v_buf1);
-    compute(b, k_buf0, v_buf0);
+    if (b + 1 < nblk) load_next(k_buf1, v_buf1, c1);
+    compute(c0, k_buf0, v_buf0);
     wait_vmem();
     __syncthreads();
     if (b + 1 < nblk) {
-      if (b + 2 < nblk) load_block(b + 2, k_buf0, v_buf0);
-      compute(b + 1, k_buf1, v_buf1);
+      if (b + 2 < nblk) load_next(k_buf0, v_buf0, c0);
+      compute(c1, k_buf1, v_buf1);
       wait_vmem();
       __syncthreads();
     }
@@ -318,60 +347,106 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   // the g heads of a block are taken one after the other, so that the
   // concurrent tiles of one KV head (causal ranges all end at the segment end;
   // the response rows of a group are the same for all its prompt key tiles)
-  // stay at the same query rows and share the Q / dO blocks in L2. The sweep
-  // steps from one block to the next with compares only (no division per
-  // block: the scalar unit is shared by the SIMDs of the CU).
-  struct Blk {
-    int y, hl, qb;  // range (0: X, 1: Y), head within the group, block (counting down)
-  };
+  // stay at the same query rows and share the Q / dO blocks in L2.
+  //
+  // The block state carries the block's source addresses and moves them by
+  // constant steps: all eight wavefronts of the workgroup step it after every
+  // barrier, on the one scalar unit of the CU, while no MFMA is ready yet, so
+  // its per-block scalar work (a few adds; the multiplies and selects happen
+  // once per range) is on the critical path of every block.
   const int g = p.group;
-  Blk first;
-  first.y = nxb > 0 ? 0 : 1;
-  first.hl = 0;
-  first.qb = (first.y ? nyb : nxb) - 1;
-  auto next_blk = [&](Blk r) -> Blk {
-    if (++r.hl == g) {
-      r.hl = 0;
-      if (--r.qb < 0 && r.y == 0) {
-        r.y = 1;
-        r.qb = nyb - 1;
-      }
-    }
-    return r;
-  };
-
+  const int64_t h0 = (int64_t)kvh * g;
+  const int64_t srx = p.lse_rows[0], sry = p.lse_rows[1];
   // Wavefront 0 loads the raw LSE and wavefront 1 the D values of the next
   // query block into `stat`; they are scaled and stored to LDS at the end of
   // the iteration, so nothing waits on these loads (or on the tile copies
   // issued before them) while the current block is computed.
+  const float* const s_base0 = (wave_u == 0 ? p.lse[0] : p.dsum[0]) + h0 * srx + t.x_row0;
+  const float* const s_base1 = (wave_u == 0 ? p.lse[1] : p.dsum[1]) + h0 * sry + t.kv_row0;
+  const int qrow_bytes = (int)(qstride * 2);
+  // The load cursor: the next block to be copied into LDS, stepped in place.
+  struct Cursor {
+    int y, hl, qb;            // range (0: X, 1: Y), head within the group, block (counting down)
+    int nvalid, nbytes;       // valid rows of the block; those rows x the row stride in bytes
+    int64_t sstep, sback;     // statistic byte steps: to the next head; from head g-1 to head 0 one block back
+    const char* qp;           // Q of the block's first row, head hl
+    const char* op;           // dO, the same
+    const char* sp;           // the statistic (LSE or D) of the block's first row, head hl
+  };
+  // bytes from head g-1 to head 0 one block back
+  const int64_t qback = ((int64_t)(g - 1) * D + KV_BQ * qstride) * 2;
+  // the last block of range y, head 0
+  auto range_start = [&](int y) {
+    Cursor r;
+    const int len = y ? t.y_len : t.x_len;
+    const int64_t srow = y ? sry : srx;
+    r.y = y;
+    r.hl = 0;
+    r.qb = (len + KV_BQ - 1) / KV_BQ - 1;
+    r.nvalid = len - r.qb * KV_BQ;
+    r.nbytes = r.nvalid * qrow_bytes;
+    r.sstep = srow * 4;
+    r.sback = ((int64_t)(g - 1) * srow + KV_BQ) * 4;
+    const int64_t row0 = (int64_t)(y ? t.kv_row0 : t.x_row0) + (int64_t)r.qb * KV_BQ;
+    const int64_t e0 = row0 * qstride + h0 * D;
+    r.qp = reinterpret_cast<const char*>(p.q[y] + e0);
+    r.op = reinterpret_cast<const char*>(p.dout[y] + e0);
+    r.sp = reinterpret_cast<const char*>((y ? s_base1 : s_base0) + r.qb * KV_BQ);
+    return r;
+  };
+  const Cursor ystart = range_start(1);
+  Cursor ld = nxb > 0 ? range_start(0) : ystart;
+  // Step to the next block in sweep order (past the end of range Y: never
+  // loaded). The pointers move by a step chosen on the (rare) head wrap and
+  // range change paths and added on the one common path, so the compiler
+  // keeps them in place instead of copying every field at the merge.
+  auto advance = [&]() {
+    int64_t dq = 2 * D, dout = 2 * D, ds = ld.sstep;
+    if (++ld.hl == g) {
+      ld.hl = 0;
+      if (ld.qb > 0) {
+        --ld.qb;
+        ld.nvalid = KV_BQ;
+        ld.nbytes = KV_BQ * qrow_bytes;
+        dq = -qback;
+        dout = -qback;
+        ds = -ld.sback;
+      } else if (ld.y == 0) {
+        dq = ystart.qp - ld.qp;
+        dout = ystart.op - ld.op;
+        ds = ystart.sp - ld.sp;
+        ld.y = 1;
+        ld.qb = ystart.qb;
+        ld.nvalid = ystart.nvalid;
+        ld.nbytes = ystart.nbytes;
+        ld.sstep = ystart.sstep;
+        ld.sback = ystart.sback;
+      }
+    }
+    ld.qp += dq;
+    ld.op += dout;
+    ld.sp += ds;
+  };
+
+  // what the computation of a block needs to know of it
+  struct Blk {
+    int y, qb;
+  };
   float stat = 0.f;
   int stat_n = 0;
   TileCopy<KV_BQ, D, 8> qc;
   qc.init(qstride);
-  // the query-side tensors of both ranges, read from the kernel arguments
-  // once (a per-block indexed read of the arguments would be a scalar load
-  // plus a wait in the loop), at the range's first row and the KV head's
-  // first query head, so that a block needs one offset
-  const int64_t h0 = (int64_t)kvh * g;
-  const int64_t xr0 = t.x_row0, yr0 = t.kv_row0;
-  const uint16_t* const qx = p.q[0] + xr0 * qstride + h0 * D;
-  const uint16_t* const qy = p.q[1] + yr0 * qstride + h0 * D;
-  const uint16_t* const ox = p.dout[0] + xr0 * qstride + h0 * D;
-  const uint16_t* const oy = p.dout[1] + yr0 * qstride + h0 * D;
-  const int64_t srx = p.lse_rows[0], sry = p.lse_rows[1];
-  const float* const sx = (wave_u == 0 ? p.lse[0] : p.dsum[0]) + h0 * srx + xr0;
-  const float* const sy = (wave_u == 0 ? p.lse[1] : p.dsum[1]) + h0 * sry + yr0;
-  auto load_block = [&](const Blk& k, __bf16* qd, __bf16* od) {
-    const int r = k.qb * KV_BQ;  // the block's first row inside its range
-    const int nvalid = min(KV_BQ, (k.y ? t.y_len : t.x_len) - r);
-    const int64_t off = (int64_t)r * qstride + k.hl * D;
-    qc.issue_at(qd, (k.y ? qy : qx) + off, nvalid, qstride);
-    qc.issue_at(od, (k.y ? oy : ox) + off, nvalid, qstride);
+  // copy the cursor's block into (qd, od), note it in k and step the cursor
+  auto load_next = [&](__bf16* qd, __bf16* od, Blk& k) {
+    qc.issue_bytes(qd, reinterpret_cast<const uint16_t*>(ld.qp), ld.nbytes);
+    qc.issue_bytes(od, reinterpret_cast<const uint16_t*>(ld.op), ld.nbytes);
     if (wave_u < 2) {
-      const float* src = (k.y ? sy : sx) + (int64_t)k.hl * (k.y ? sry : srx) + r;
-      stat = src[min(lane, nvalid - 1)];
-      stat_n = nvalid;
+      stat = reinterpret_cast<const float*>(ld.sp)[min(lane, ld.nvalid - 1)];
+      stat_n = ld.nvalid;
     }
+    k.y = ld.y;
+    k.qb = ld.qb;
+    advance();
   };
   // stored as the S and dP accumulator start values -LSE / scale and -D
   // (-inf past the end of the range, so those rows get P = 0)
@@ -381,7 +456,6 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     else if (wave_u == 1) dd[lane] = lane < stat_n ? -stat : 0.f;
   };
 
-  const int key_pos = t.kpos0 + kj;  // this lane's key position (causal ranges)
   RowOffsets<D> qrow_off, key_off;   // Q/dO rows of this wave's half; K/V rows of its keys
   qrow_off.init(qs * 32 + l32, hf);
   key_off.init(kj, hf);
@@ -392,11 +466,14 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
   TrOffsets<D> qtr_off;              // Q^T / dO^T operands of this wave's half
   qtr_off.init(qs * 32, lane);
   auto compute = [&](const Blk& k, const __bf16* ql, const __bf16* dl, const float* lsel, const float* dsl) {
-    const bool causal = k.y || x_causal;
-    const int qpos0 = t.kpos0 + k.qb * KV_BQ + qs * 32;  // position of this wave's first query (causal)
-    const bool skip = causal && (qpos0 + 31 < t.kpos0 + kw0);
-    if (skip) return;
-    const bool need_mask = causal && (qpos0 < t.kpos0 + kw0 + 31);
+    // A causal range starts at the tile's first key position, so only its
+    // blocks 0 and 1 (rows 0 .. 127) reach the diagonal of the 128 keys.
+    const int qrel = k.qb * KV_BQ + qs * 32 - kw0;  // this wave's first query row - its first key
+    bool need_mask = false;
+    if (k.qb < 2 && (k.y || x_causal)) {
+      if (qrel + 31 < 0) return;  // every key of the wave after every row
+      need_mask = qrel < 31;
+    }
     // S and dP accumulators start at -LSE / scale and -D of their rows
     // (register i holds row g4 * 8 + 4 * hf + e, i = 4 * g4 + e), so the
     // MFMAs leave S - LSE / scale and dP - D: P = exp2(c * s), dS = P * dp.
@@ -422,7 +499,7 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     if (need_mask) {  // only blocks that cross the diagonal
 #pragma unroll
       for (int i = 0; i < 16; ++i)
-        if (key_pos > qpos0 + acc_row(i, hf)) s[i] = -INFINITY;
+        if (l32 > qrel + acc_row(i, hf)) s[i] = -INFINITY;
     }
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
@@ -444,28 +521,25 @@ __global__ __launch_bounds__(512) void attn_dkv_kernel(DkvParams p) {
     set_wave_priority<1>();
   };
 
-  Blk cur = first;
+  Blk c0{0, 0}, c1{0, 0};
   if (nblk > 0) {
-    load_block(cur, q_buf0, o_buf0);
+    load_next(q_buf0, o_buf0, c0);
     store_stat(nlse_buf0, ndsum_buf0);
   }
   wait_vmem();
   __syncthreads();
   for (int b = 0; b < nblk; b += 2) {
-    const Blk b1 = next_blk(cur);
-    if (b + 1 < nblk) load_block(b1, q_buf1, o_buf1);
-    compute(cur, q_buf0, o_buf0, nlse_buf0, ndsum_buf0);
+    if (b + 1 < nblk) load_next(q_buf1, o_buf1, c1);
+    compute(c0, q_buf0, o_buf0, nlse_buf0, ndsum_buf0);
     if (b + 1 < nblk) store_stat(nlse_buf1, ndsum_buf1);
     wait_vmem();
     __syncthreads();
     if (b + 1 < nblk) {
-      const Blk b2 = next_blk(b1);
-      if (b + 2 < nblk) load_block(b2, q_buf0, o_buf0);
-      compute(b1, q_buf1, o_buf1, nlse_buf1, ndsum_buf1);
+      if (b + 2 < nblk) load_next(q_buf0, o_buf0, c0);
+      compute(c1, q_buf1, o_buf1, nlse_buf1, ndsum_buf1);
       if (b + 2 < nblk) store_stat(nlse_buf0, ndsum_buf0);
       wait_vmem();
       __syncthreads();
-      cur = b2;
     }
   }
 

@@ -204,9 +204,11 @@ struct TileCopy {
   static constexpr int PER_WAVE = (NI + NWAVES - 1) / NWAVES;
   static_assert(ROWS % RPI == 0, "tile rows");
   uint32_t off[PER_WAVE];  // byte offset of this lane's chunk inside a block of rows
+  int wave;                // this wavefront's index (uniform)
 
   __device__ __forceinline__ void init(int64_t stride) {
-    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int lane = threadIdx.x & 63;
+    wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
 #pragma unroll
     for (int k = 0; k < PER_WAVE; ++k) {
       const int i = wave + k * NWAVES;
@@ -223,17 +225,21 @@ struct TileCopy {
   }
   // the same from the address of the first row's first column
   __device__ __forceinline__ void issue_at(__bf16* lds, const uint16_t* gb, int nvalid, int64_t stride) const {
+    const int rows = nvalid < ROWS ? nvalid : ROWS;
+    issue_bytes(lds, gb, (int)(rows * stride * 2));
+  }
+  // the same with the valid range given in bytes from gb (nbytes: the rows
+  // that are read times the row stride in bytes; at most 2^31 - 1)
+  __device__ __forceinline__ void issue_bytes(__bf16* lds, const uint16_t* gb, int nbytes) const {
     // Device pass only: with a buffer-resource value in a kernel body, the
     // host pass silently drops the launch stubs of some instantiations.
 #if defined(__HIP_DEVICE_COMPILE__)
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int rows = nvalid < ROWS ? nvalid : ROWS;
-    const __amdgpu_buffer_rsrc_t rsrc =
-        __builtin_amdgcn_make_buffer_rsrc((void*)gb, 0, (int)(rows * stride * 2), 0x00020000);
+    const __amdgpu_buffer_rsrc_t rsrc = __builtin_amdgcn_make_buffer_rsrc((void*)gb, 0, nbytes, 0x00020000);
 #pragma unroll
     for (int k = 0; k < PER_WAVE; ++k) {
       const int i = wave + k * NWAVES;
-      if (i < NI)
+      // every wavefront has PER_WAVE instructions when NWAVES divides NI
+      if (NI % NWAVES == 0 || i < NI)
         __builtin_amdgcn_raw_ptr_buffer_load_lds(rsrc, (__attribute__((address_space(3))) void*)(lds + i * RPI * D),
                                                  16, off[k], 0, 0, 0);
     }
