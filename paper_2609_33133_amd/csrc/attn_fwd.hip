@@ -135,14 +135,24 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
         if (acc_row(i, hf) + 32 > lim) s1[i] = -INFINITY;
       }
     }
-    // four independent max chains, then a tree (short dependency chains),
-    // and the half-wave exchange without LDS
+    // four independent chains of three-input maxima (v_max3_f32, written
+    // out: left to itself the compiler pairs the values with two-input maxima
+    // first and needs about a third more instructions), and the half-wave
+    // exchange without LDS
+    auto max3 = [](float a, float b, float c) {
+      float r;
+      asm("v_max3_f32 %0, %1, %2, %3" : "=v"(r) : "v"(a), "v"(b), "v"(c));
+      return r;
+    };
     float m4[4];
 #pragma unroll
-    for (int j = 0; j < 4; ++j) m4[j] = fmaxf(s0[j], s1[j]);
-#pragma unroll
-    for (int i = 4; i < 16; ++i) m4[i & 3] = fmaxf(m4[i & 3], fmaxf(s0[i], s1[i]));
-    const float mx = pair_max(fmaxf(fmaxf(m4[0], m4[1]), fmaxf(m4[2], m4[3])));
+    for (int j = 0; j < 4; ++j) {
+      float m = max3(s0[j], s1[j], s0[j + 4]);
+      m = max3(m, s1[j + 4], s0[j + 8]);
+      m = max3(m, s1[j + 8], s0[j + 12]);
+      m4[j] = fmaxf(m, s1[j + 12]);
+    }
+    const float mx = pair_max(fmaxf(max3(m4[0], m4[1], m4[2]), m4[3]));
     const float mnew = fmaxf(m_run, mx);
     // rescale only when some row maximum of this wavefront passed its
     // reference by more than the margin (always on a row's first visible key:
