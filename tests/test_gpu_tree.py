@@ -13,7 +13,7 @@ from paper_2609_33133_amd import inputs as I
 from paper_2609_33133_amd.api import REPLAY_AUTO, REPLAY_FUSED, REPLAY_SPLIT, GroupBatch
 from paper_2609_33133_amd.group_attention import SharedStep, upload
 
-from gpu_helpers import log, rel
+from gpu_helpers import assert_close, log, oracle, rel, run_shared
 
 pytestmark = pytest.mark.gpu
 
@@ -125,3 +125,25 @@ def test_tree_chunked_prompt_sweeps(case, chunk):
     a2 = tree.outputs()
     for k in ("dk_p", "dv_p", "dq_p", "dq_r"):
         assert torch.equal(a[k].view(torch.uint8), a2[k].view(torch.uint8)), k
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_tree_random_shapes_against_oracle(seed):
+    """Random ragged batches (up to 3 trees, 6 branches, GQA g = 1, 4, 7, 8,
+    d = 64 and 128, normal and sharp logits) through the two-call step, with
+    the default sweeps and with prompt-key sweeps cut into 3-block chunks,
+    each against the fp64 oracle."""
+    rng = np.random.default_rng(5000 + seed)
+    shape = I.random_shape(rng, max_groups=3, max_p=700, max_g=6, max_r=500,
+                           heads=((4, 4, 64), (8, 2, 128), (4, 1, 128), (28, 4, 128), (16, 2, 64), (8, 8, 128)))
+    gi = I.make_inputs(shape, seed=6000 + seed, qk_mult=[None, 1.0, 2.0][seed % 3])
+    log(f"[tree random] seed {seed}: P={shape.prompt_lens} R={shape.branch_lens} "
+        f"h={shape.num_q_heads}/{shape.num_kv_heads} d={shape.head_dim}")
+    ref = oracle(gi)
+    for chunk in (0, 3):
+        api.set_tree_chunk_blocks(chunk)
+        try:
+            got, _ = run_shared(gi, mode=REPLAY_AUTO)
+        finally:
+            api.set_tree_chunk_blocks(0)
+        assert_close(got, ref, f"tree random {seed} chunk {chunk}")
