@@ -46,7 +46,8 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   __shared__ __bf16 k_buf0[BN * D], k_buf1[BN * D], v_buf0[BN * D], v_buf1[BN * D];
   int unit, hh;
   if (!xcd_unit(p.n_units, p.group, unit, hh)) return;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6, l32 = lane & 31, hf = lane >> 5;
+  const int tid = threadIdx.x, lane = tid & 63, l32 = lane & 31, hf = lane >> 5;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);  // uniform: scalar branches below
   const int tile_id = unit / p.hkv;
   const int kvh = unit - tile_id * p.hkv;
   const int head = kvh * p.group + hh;
@@ -86,19 +87,37 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
 
   TileCopy<BN, D, 4> cp;
   cp.init(kvstride);
-  // K / V of both segments at the segment's first row and this KV head, so
-  // that a block needs one offset
-  const uint16_t* const ka0 = p.ka + (int64_t)t.a_row0 * kvstride + kvh * D;
-  const uint16_t* const va0 = p.va + (int64_t)t.a_row0 * kvstride + kvh * D;
-  const uint16_t* const kb0p = kb + (int64_t)t.b_row0 * kvstride + kvh * D;
-  const uint16_t* const vb0p = vb + (int64_t)t.b_row0 * kvstride + kvh * D;
-  auto load = [&](int b, bool val, __bf16* dst) {
-    const bool isB = b >= nA;
-    const int kb0 = (isB ? b - nA : b) * BN;
-    const int len = isB ? t.b_len : t.a_len;
-    const uint16_t* src = val ? (isB ? vb0p : va0) : (isB ? kb0p : ka0);
-    cp.issue_at(dst, src + (int64_t)kb0 * kvstride, min(BN, len - kb0), kvstride);
+  // K / V of both segments at the segment's first row and this KV head
+  const char* const ka0 = reinterpret_cast<const char*>(p.ka + (int64_t)t.a_row0 * kvstride + kvh * D);
+  const char* const va0 = reinterpret_cast<const char*>(p.va + (int64_t)t.a_row0 * kvstride + kvh * D);
+  const char* const kb0p = reinterpret_cast<const char*>(kb + (int64_t)t.b_row0 * kvstride + kvh * D);
+  const char* const vb0p = reinterpret_cast<const char*>(vb + (int64_t)t.b_row0 * kvstride + kvh * D);
+  // Load cursors of K and V: the next block of each to be copied into LDS,
+  // stepped in place, so that a block's scalar work is a few adds (the
+  // eight wavefronts of a CU share one scalar unit)
+  struct KvCursor {
+    int isB, kb0, len;  // segment (0: A, 1: B), the block's first key in it, the segment's length
+    const char* src;    // the block's first key row, KV head kvh
   };
+  const int row_bytes = (int)(kvstride * 2);
+  KvCursor kcur = nA > 0 ? KvCursor{0, 0, t.a_len, ka0} : KvCursor{1, 0, t.b_len, kb0p};
+  KvCursor vcur = nA > 0 ? KvCursor{0, 0, t.a_len, va0} : KvCursor{1, 0, t.b_len, vb0p};
+  // copy the cursor's block into dst and step the cursor (past the end of
+  // segment B: never loaded)
+  auto load_next = [&](KvCursor& c, const char* seg_b, __bf16* dst) {
+    cp.issue_bytes(dst, reinterpret_cast<const uint16_t*>(c.src), min(BN, c.len - c.kb0) * row_bytes);
+    int64_t step = (int64_t)BN * row_bytes;
+    c.kb0 += BN;
+    if (c.kb0 >= c.len && c.isB == 0) {
+      step = seg_b - c.src;
+      c.isB = 1;
+      c.kb0 = 0;
+      c.len = t.b_len;
+    }
+    c.src += step;
+  };
+  auto load_k = [&](__bf16* dst) { load_next(kcur, kb0p, dst); };
+  auto load_v = [&](__bf16* dst) { load_next(vcur, vb0p, dst); };
 
   RowOffsets<D> k_off;  // K row l32; row 32 + l32 has the same swizzle, 32 rows further
   k_off.init(l32, hf);
@@ -179,12 +198,12 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
     const float ms = stats(b, s0, s1);
     __builtin_amdgcn_sched_barrier(0);
     s_mfma(kn, n0, n1);
-    float l4[4] = {0.f, 0.f, 0.f, 0.f};  // four independent partial sums
+    float l4[4];  // four independent partial sums
 #pragma unroll
     for (int i = 0; i < 16; ++i) {
       s0[i] = __builtin_amdgcn_exp2f(s0[i] * c - ms);
       s1[i] = __builtin_amdgcn_exp2f(s1[i] * c - ms);
-      l4[i & 3] += s0[i] + s1[i];
+      l4[i & 3] = i < 4 ? s0[i] + s1[i] : l4[i & 3] + (s0[i] + s1[i]);
     }
     l_run += (l4[0] + l4[1]) + (l4[2] + l4[3]);
     const bf16x8 pb0 = to_bf16x8(s0, 0), pb1 = to_bf16x8(s0, 8);
@@ -217,9 +236,9 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   // loads K(b + 2) over K(b) and V(b + 1) over V(b - 1).
   f32x16 sa0, sa1, sb0, sb1;
   if (nblk > 0) {
-    load(0, false, k_buf0);
-    load(0, true, v_buf0);
-    if (nblk > 1) load(1, false, k_buf1);
+    load_k(k_buf0);
+    load_v(v_buf0);
+    if (nblk > 1) load_k(k_buf1);
   }
   wait_vmem();
   __syncthreads();
@@ -227,14 +246,14 @@ __global__ __launch_bounds__(256, 2) void attn_fwd_kernel(FwdParams p) {
   pace_lds_mfma<D / 8, 1, FWD_DEPTH>();
   __syncthreads();
   for (int b = 0; b < nblk; b += 2) {
-    if (b + 2 < nblk) load(b + 2, false, k_buf0);
-    if (b + 1 < nblk) load(b + 1, true, v_buf1);
+    if (b + 2 < nblk) load_k(k_buf0);
+    if (b + 1 < nblk) load_v(v_buf1);
     if (!skipped(b)) step(b, sa0, sa1, k_buf1, v_buf0, sb0, sb1);
     wait_vmem();
     __syncthreads();
     if (b + 1 < nblk) {
-      if (b + 3 < nblk) load(b + 3, false, k_buf1);
-      if (b + 2 < nblk) load(b + 2, true, v_buf0);
+      if (b + 3 < nblk) load_k(k_buf1);
+      if (b + 2 < nblk) load_v(v_buf0);
       if (!skipped(b + 1)) step(b + 1, sb0, sb1, k_buf0, v_buf1, sa0, sa1);
       wait_vmem();
       __syncthreads();
