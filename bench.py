@@ -130,8 +130,9 @@ WORKLOAD_SLUG = {"tiny": "tiny_P256_G2", "balanced": "balanced_4groups_P4096_G8"
 
 def kernel_source_hash() -> str:
     """Hash of the code (comments and whitespace removed) of every native
-    source the kernels and their schedules are built from: HBM counters
-    recorded under one hash do not describe another."""
+    source the kernels and their schedules are built from, and of the
+    compile flags: HBM counters recorded under one hash do not describe
+    another."""
     h = hashlib.sha256()
     for path in sorted(glob.glob(os.path.join(ROOT, "paper_2609_33133_amd", "csrc", "*"))):
         if path.endswith((".hip", ".h", ".cpp")):
@@ -141,6 +142,9 @@ def kernel_source_hash() -> str:
             code = re.sub(r"//[^\n]*", " ", code)
             h.update(os.path.basename(path).encode())
             h.update(" ".join(code.split()).encode())
+    from paper_2609_33133_amd import build as _build
+    for src in ("attn_fwd.hip", "attn_bwd.hip", "elementwise.hip"):
+        h.update(" ".join(_build.hip_flags(src)).encode())
     return h.hexdigest()[:16]
 
 

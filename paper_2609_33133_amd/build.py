@@ -25,6 +25,15 @@ ARCH = "gfx950"
 COMMON = ["-O3", "-std=c++17", "-fPIC", "-I" + os.path.join(ROOT, "include"), "-I" + CSRC, "-I/opt/rocm/include"]
 HIP_FLAGS = ["--offload-arch=" + ARCH, "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops", "-fno-honor-nans",
              "-ffp-contract=fast"]
+# The attention kernels are scheduled by the backend's instruction-level
+# parallelism strategy (the dK/dV kernel runs ~1 % faster than with the
+# default occupancy-driven one, the other two slightly faster; no spills);
+# the bandwidth-bound merge and reduce kernels keep the default.
+ATTN_FLAGS = ["-mllvm", "-amdgpu-sched-strategy=max-ilp"]
+
+
+def hip_flags(src: str):
+    return HIP_FLAGS + (ATTN_FLAGS if os.path.basename(src).startswith("attn_") else [])
 
 
 def hipcc() -> str:
@@ -49,7 +58,7 @@ def build(verbose: bool = False) -> str:
     jobs = []
     for src in sorted(glob.glob(os.path.join(CSRC, "*.hip"))):
         obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-        jobs.append(([cc, "-x", "hip", *HIP_FLAGS, *COMMON, "-c", src, "-o", obj], obj))
+        jobs.append(([cc, "-x", "hip", *hip_flags(src), *COMMON, "-c", src, "-o", obj], obj))
     for src in sorted(glob.glob(os.path.join(CSRC, "*.cpp"))):
         obj = os.path.join(BUILD, os.path.basename(src) + ".o")
         jobs.append(([cc, "-x", "c++", "-D__HIP_PLATFORM_AMD__", *COMMON, "-c", src, "-o", obj], obj))
