@@ -66,6 +66,18 @@ def test_recorded_traffic_requires_matching_sources(tmp_path, monkeypatch):
     assert bench.recorded_traffic("prompt", "attn_dq_kernel", "calls") is None   # counters of the other path
 
 
+def test_source_hash_covers_compile_flags(monkeypatch):
+    """Recorded counters describe one build: a change of the attention
+    sources' compile flags changes the hash, so their traffic is no longer
+    reported."""
+    from paper_2609_33133_amd import build
+    h0 = bench.kernel_source_hash()
+    assert "-amdgpu-sched-strategy=max-ilp" in " ".join(build.hip_flags("attn_bwd.hip"))
+    assert "-amdgpu-sched-strategy=max-ilp" not in " ".join(build.hip_flags("elementwise.hip"))
+    monkeypatch.setattr(build, "ATTN_FLAGS", [])
+    assert bench.kernel_source_hash() != h0
+
+
 def test_trace_summary(tmp_path):
     p = tmp_path / "stats.csv"
     with open(p, "w", newline="") as f:
